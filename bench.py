@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark: fused sharded AdamW commit + state digest on one MI355X.
+
+One step = one commit of the whole shard (read p, g, m, v; write p', m', v'
+and the bf16 copy; digest of the committed state in the same pass).  Default
+workload: the 453,001,472-element 1/16 FSDP shard of Mistral-7B at rank 15
+(flat indices beyond 2^32), warm AdamW state at step 5.  Inputs are
+synthetic, drawn by the seeded generator in ``workloads`` and resident in HBM
+before timing starts.
+
+Prints one JSON line.  ``value`` is elements committed per second;
+``roofline`` prices the commit kernel against MI355X's 8 TB/s HBM peak at
+30 algorithmic bytes per element; ``cpu_baseline`` times the CPU oracle on a
+bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "shard commit+digest elements/s and HBM GB/s (% of MI355X peak), 1 GPU"
+PEAK_HBM_GBPS = 8000.0
+BYTES_PER_ELEM = 30  # read p, g, m, v (16) + write p', m', v' (12) + bf16 (2)
+KERNEL_SOURCES = ("paper_2609_18178_amd/csrc/kernels.hip", "paper_2609_18178_amd/csrc/launch.h")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mistral7b_shard16")
+    ap.add_argument("--cpu-seconds", type=float, default=6.0,
+                    help="target seconds for each CPU oracle leg (single thread, all threads)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probe", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, seconds: float) -> dict:
+    """The oracle, unchanged, on a bounded sample: the first 2^24 elements of
+    the same shard.  Leg 1: one thread.  Leg 2: the sample cut into one slice
+    per host thread (the digest of the whole is the wrapping sum of the
+    slices).  Each leg repeats commits until `seconds` have passed."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+    import workloads as wl
+
+    n = min(1 << 24, w.numel)
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    b = np.zeros(n, np.uint16)
+    h = oracle.Hyper(**(w.hypers[0]))
+
+    def leg(threads):
+        cuts = [n * k // threads for k in range(threads + 1)]
+
+        def one(args):
+            k, step = args
+            a, z = cuts[k], cuts[k + 1]
+            return oracle.commit_and_digest(p[a:z], g[a:z], m[a:z], v[a:z], b[a:z], h, step, w.global_offset + a)
+
+        done, step, t0 = 0, w.first_step, time.perf_counter()
+        with ThreadPoolExecutor(threads) as ex:
+            while True:
+                list(ex.map(one, [(k, step) for k in range(threads)]))
+                done += n
+                step += 1
+                el = time.perf_counter() - t0
+                if el >= seconds:
+                    return done / el
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    single = leg(1)
+    multi = leg(threads)
+    return {
+        "value": multi,
+        "unit": "elements/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"first {n} elements of the {w.name} shard (same offset, distributions and step), "
+                  f"commit+digest repeated for >= {seconds:g} s per leg; the oracle cut into {threads} slices "
+                  f"run by {threads} threads",
+        "single_thread_value": single,
+        "cpu_model": platform.processor() or _cpu_model(),
+    }
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def stored_traffic(workload: str, src_hash: str):
+    """HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs of the
+    current kernel source, if such a record exists."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != src_hash:
+        return None
+    return rec
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the commit of a "
+              "rank's shard needs no communication, and sharding across GPUs is not part of this build.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_18178_amd as pk
+    import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    if w.segments is not None:
+        segments = list(w.segments)
+        hypers = [pk.Hyper(**h) for h in w.hypers]
+    else:
+        segments, hypers = None, None
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n = w.numel
+    t_setup = time.perf_counter()
+    tensors = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(4)]
+    for t, aid, step, dist in zip(tensors, (wl.ARRAY_PARAM, wl.ARRAY_GRAD, wl.ARRAY_EXP_AVG, wl.ARRAY_EXP_AVG_SQ),
+                                  (0, w.first_step, 0, 0), (w.param, w.grad, w.exp_avg, w.exp_avg_sq)):
+        wl.fill_device(t, w.global_offset, w.seed, aid, step, dist)
+    bf16 = torch.zeros(n, dtype=torch.int16, device=dev)
+    sh = pk.Shard(*tensors, bf16, global_offset=w.global_offset, segments=segments, hypers=hypers)
+    hyper = None if segments else pk.Hyper(**w.hypers[0])
+    setup_s = time.perf_counter() - t_setup
+    print(f"[bench] {w.name}: {n} elements resident ({setup_s:.1f} s setup)", file=sys.stderr, flush=True)
+
+    step = w.first_step
+    for _ in range(args.warmup):
+        pk.adamw_commit(sh, step, hyper)
+        step += 1
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    region_s, region_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    region_s.record()
+    for k in range(K):
+        ev_s[k].record()
+        pk.adamw_commit(sh, step, hyper)
+        ev_e[k].record()
+        step += 1
+    region_e.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = region_s.elapsed_time(region_e)
+    per_launch_ms = [a.elapsed_time(b) for a, b in zip(ev_s, ev_e)]
+    last_digest = pk.to_u64(sh.digest)[-1]
+    ms_per_step = total_ms / K
+    avg_launch_ms = sum(per_launch_ms) / K
+    value = n / (ms_per_step / 1e3)
+    algo_bytes = BYTES_PER_ELEM * n
+    achieved = algo_bytes / (avg_launch_ms / 1e3) / 1e9
+    print(f"[bench] {K} commits: {ms_per_step:.4f} ms/step, kernel {avg_launch_ms:.4f} ms avg "
+          f"(min {min(per_launch_ms):.4f}), {achieved:.1f} GB/s", file=sys.stderr, flush=True)
+
+    probe = None
+    if not args.no_probe and segments is None:
+        p_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+        p_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+        for k in range(K):
+            p_s[k].record()
+            pk.stream_probe(tensors[0], tensors[1], tensors[2], tensors[3], tensors[0], tensors[2], tensors[3], bf16)
+            p_e[k].record()
+        torch.cuda.synchronize()
+        pms = sum(a.elapsed_time(b) for a, b in zip(p_s, p_e)) / K
+        probe = {"kernel": "stream_probe", "ms": pms, "gbps": algo_bytes / (pms / 1e3) / 1e9,
+                 "frac_of_peak": algo_bytes / (pms / 1e3) / 1e9 / PEAK_HBM_GBPS}
+        print(f"[bench] stream probe (same 30 B/element, no math): {probe['gbps']:.1f} GB/s",
+              file=sys.stderr, flush=True)
+
+    src_hash = kernel_source_hash()
+    traffic_rec = stored_traffic(w.name, src_hash)
+    traffic = None if traffic_rec is None else traffic_rec["bytes_per_launch"]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Philox4x32-10 inputs with the workload's shapes and distributions)",
+        "config": dict(w.describe(), parallelism="one rank's shard, no collectives",
+                       bytes_per_element=BYTES_PER_ELEM),
+        "hbm_gbps_nominal": algo_bytes / (ms_per_step / 1e3) / 1e9,
+        "pct_of_peak_hbm": 100.0 * algo_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "shard_kernel<Commit>",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": algo_bytes,
+            "avg_launch_ms": avg_launch_ms,
+            "timing": "hipEvents around each commit call on the launch stream (includes the digest-slot "
+                      "zeroing kernel, about 2 us)",
+        },
+        "cpu_baseline": cpu,
+        "probe": probe,
+        "kernel_source_hash": src_hash,
+        "last_digest": f"{last_digest:#018x}",
+        "wall_s_timed_region": wall,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,155 @@
+/*
+ * pactshard.h -- C ABI of libpactshard: the per-rank sharded AdamW commit and
+ * the 64-bit state digest, for AMD Instinct MI355X (gfx950).
+ *
+ * What the calls compute.  The preserved training state of a rank is its
+ * shard of the weights W, the AdamW moments M and V, and the optimizer step
+ * counter (Sec. III-A, eq. 2).  In-memory recovery keeps that state in device
+ * memory once the optimizer update has committed (Sec. I; Sec. III-A, action
+ * L1), and every rank must then hold it bit-identically (abstract; Sec. IV-G).
+ * pact_adamw_commit applies that update to one flat shard; pact_shard_digest
+ * names the committed state in 64 bits so ranks can compare it cheaply.
+ *
+ * Arithmetic (the paper prints no formula; this is the library's contract).
+ * Per call, per segment, in double and rounded once to binary32:
+ *   decay = 1 - lr*wd, omb1 = 1 - beta1, omb2 = 1 - beta2,
+ *   step_size = lr / (1 - beta1^t), rs_bc2 = 1 / sqrt(1 - beta2^t),
+ * with beta^t formed by t successive double multiplications.  Per element,
+ * each operation one binary32 round-to-nearest-even, no fused multiply-add:
+ *   p1 = p*decay;  m' = beta1*m + omb1*g;  v' = beta2*v + omb2*(g*g);
+ *   den = sqrt(v')*rs_bc2 + eps;  p' = p1 - step_size*(m'/den)
+ * with IEEE-correct sqrt and division and fp32 denormals kept.  The bf16 copy
+ * is round-to-nearest-even of p' (NaN: quiet, sign and top payload kept).
+ *
+ * Digest.  D = sum over k in {0:p', 1:m', 2:v'} and shard elements i of
+ *   splitmix64( zext64(bits32(X_k[i])) XOR ((global_offset + i) | k << 56) )
+ * mod 2^64, where splitmix64(x) is the generator output for state x (add the
+ * golden gamma 0x9E3779B97F4A7C15, then the standard 30/27/31 mix).  The sum
+ * wraps, so D does not depend on how the index range is partitioned: digests
+ * of disjoint shards, segments or ranks add up to the digest of their union.
+ * The bf16 digest uses tag k = 3 on the zero-extended 16-bit words.
+ *
+ * Memory and ownership.  Every buffer belongs to the caller; the library
+ * allocates nothing.  All array pointers are device pointers (HBM).
+ * param, exp_avg, exp_avg_sq are read and overwritten in place; grad is only
+ * read; param_bf16 is only written.  The five arrays must not overlap each
+ * other or digest_dev.  fp32 arrays need 4-byte and bf16 2-byte alignment;
+ * a segment whose start is 16-byte aligned in all four fp32 arrays and 8-byte
+ * aligned in the bf16 array runs the vector path, any other segment the
+ * element-wise path, with identical results.
+ *
+ * Segments.  segs == NULL: the shard is one segment [0, numel) updated with
+ * *hyper, and digest_dev[0] receives D.  Otherwise segs[0..num_segs) lists
+ * disjoint ranges (offset, length, hyper_index) in increasing offset order
+ * inside [0, numel); elements outside every segment (padding) are neither
+ * read, written nor digested; hypers[hyper_index] applies per segment and
+ * `hyper` is ignored; digest_dev[0..num_segs) receive the per-segment digests
+ * and digest_dev[num_segs] their sum.  pact_digest_slots() gives the count.
+ *
+ * Streams and completion.  Every call only enqueues work on `stream` (a
+ * hipStream_t; NULL is the default stream) and returns; the digest slots
+ * hold their value once the stream has reached that point.  Calls on one
+ * stream are ordered; concurrent calls on different streams must not touch
+ * the same buffers.
+ *
+ * Errors.  0 on success, a negative PACT_E* code otherwise.  Argument errors
+ * are found before anything is enqueued and leave every buffer untouched.
+ * PACT_EHIP means a launch failed after validation: the shard may be partly
+ * updated and must be treated as uncommitted (the caller falls back to
+ * restart from a checkpoint, the paper's L2 action, Sec. III-A).
+ */
+#ifndef PACTSHARD_H
+#define PACTSHARD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PACT_OK 0
+#define PACT_EINVAL (-1)   /* null pointer, bad size, bad hyperparameter or segment table, step == 0 */
+#define PACT_EALIGN (-2)   /* misaligned pointer */
+#define PACT_EOVERLAP (-3) /* two buffers overlap */
+#define PACT_ERANGE (-4)   /* an index reaches 2^56 (the tag bits): global_offset + numel > 2^56 */
+#define PACT_EHIP (-5)     /* a HIP call failed; see pact_last_hip_error() */
+
+/* AdamW hyperparameters.  Valid: lr >= 0, 0 <= beta1 < 1, 0 <= beta2 < 1,
+ * eps > 0, weight_decay >= 0, all finite. */
+typedef struct pact_hyper {
+    float lr;
+    float beta1;
+    float beta2;
+    float eps;
+    float weight_decay;
+} pact_hyper;
+
+/* One tensor of a multi-tensor flat shard, in shard elements. */
+typedef struct pact_segment {
+    uint64_t offset;
+    uint64_t length;
+    uint32_t hyper_index;
+    uint32_t reserved; /* must be 0 */
+} pact_segment;
+
+/* One rank's flat shard.  Host struct; array pointers are device pointers,
+ * segs and hypers are host pointers read during the call only. */
+typedef struct pact_shard {
+    float* param;            /* W: fp32 master weights, numel elements          */
+    const float* grad;       /* fp32 gradient, numel elements                   */
+    float* exp_avg;          /* M: fp32 first moment                            */
+    float* exp_avg_sq;       /* V: fp32 second moment                           */
+    uint16_t* param_bf16;    /* bf16 working copy of W (bit patterns)           */
+    uint64_t numel;          /* elements in the shard, padding included         */
+    uint64_t global_offset;  /* flat index of element 0 in the full vector      */
+    const pact_segment* segs;/* NULL or num_segs entries                        */
+    uint32_t num_segs;
+    uint32_t num_hypers;
+    const pact_hyper* hypers;/* num_hypers entries when segs != NULL            */
+    uint64_t* digest_dev;    /* device, pact_digest_slots() uint64 slots        */
+    void* stream;            /* hipStream_t                                     */
+} pact_shard;
+
+/* Number of uint64 digest slots a call on this shard writes: 1 without
+ * segments, num_segs + 1 with them; negative error code if s is NULL. */
+int64_t pact_digest_slots(const pact_shard* s);
+
+/* The fused commit (Sec. III-A: the update after which W, M, V count as
+ * committed): reads p, g, m, v once, writes p', m', v' in place and the bf16
+ * copy, and accumulates the digest of (p', m', v') in the same pass.
+ * step = the optimizer step t >= 1 after its increment. */
+int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper);
+
+/* Digest of the current (p, m, v) without updating them (the bitwise state
+ * check of Sec. IV-G, as a 64-bit identity).  grad and param_bf16 are not
+ * read and may be NULL. */
+int pact_shard_digest(const pact_shard* s);
+
+/* Digest (tag 3) of the bf16 copy into dev_out (pact_digest_slots() slots,
+ * device memory); param, grad, exp_avg, exp_avg_sq are not read and may be
+ * NULL.  A verification aid: the bf16 copy is a function of p'. */
+int pact_bf16_digest(const pact_shard* s, uint64_t* dev_out);
+
+/* Measurement support, not part of the commit: streams the same bytes as a
+ * commit (reads 4 fp32 arrays, writes 3 fp32 arrays and one 16-bit array,
+ * 30 bytes per element) with no arithmetic beyond one add, so its rate is
+ * the practical HBM ceiling of that access pattern.  out_* may alias in_*
+ * element for element (in-place), as in a commit. */
+int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3,
+                      float* out0, float* out2, float* out3, uint16_t* out_half,
+                      uint64_t n, void* stream);
+
+/* Static text for a PACT_E* code. */
+const char* pact_strerror(int code);
+
+/* The hipError_t of the last failed HIP call on this thread (0 if none). */
+int pact_last_hip_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int pact_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PACTSHARD_H */

@@ -1,0 +1,236 @@
+"""paper_2609_18178_amd -- MI355X (gfx950) sharded AdamW commit and state digest.
+
+A thin ctypes binding over ``libpactshard.so`` (C ABI in ``include/pactshard.h``).
+Each call marshals torch tensors into a ``pact_shard`` and enqueues the
+library's kernels on torch's current HIP stream; every step of the commit and
+of the digest runs in those kernels.  torch supplies device memory and
+streams only.  There is no fallback: if the library is missing or the tensors
+are not on a GPU, the call raises.
+
+The state these calls act on is a rank's preserved training state: its shard
+of the weights W, the AdamW moments M and V and the step counter
+(Sec. III-A, eq. 2).  ``adamw_commit`` applies the update after which that
+state counts as committed (Sec. I; Sec. III-A, action L1); ``shard_digest``
+names it in 64 bits for the bitwise cross-rank state checks of Sec. IV-G.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+__all__ = [
+    "Hyper", "Shard", "PactError", "adamw_commit", "shard_digest", "bf16_digest", "stream_probe",
+    "digest_slots", "to_u64", "library_path",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libpactshard.so")
+
+MASK64 = (1 << 64) - 1
+
+PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP = 0, -1, -2, -3, -4, -5
+
+
+class PactError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {_strerror(code)} (code {code}"
+                         + (f", hip error {_lib().pact_last_hip_error()}" if code == PACT_EHIP else "") + ")")
+
+
+class _CHyper(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay")]
+
+
+class _CSegment(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_uint64), ("length", ctypes.c_uint64),
+                ("hyper_index", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+class _CShard(ctypes.Structure):
+    _fields_ = [
+        ("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+        ("exp_avg_sq", ctypes.c_void_p), ("param_bf16", ctypes.c_void_p),
+        ("numel", ctypes.c_uint64), ("global_offset", ctypes.c_uint64),
+        ("segs", ctypes.POINTER(_CSegment)), ("num_segs", ctypes.c_uint32), ("num_hypers", ctypes.c_uint32),
+        ("hypers", ctypes.POINTER(_CHyper)), ("digest_dev", ctypes.c_void_p), ("stream", ctypes.c_void_p),
+    ]
+
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(library_path):
+            raise RuntimeError(
+                f"libpactshard.so not built at {library_path}: run `make` (or __graft_entry__.build()). "
+                "There is no fallback implementation."
+            )
+        lib = ctypes.CDLL(library_path)
+        P = ctypes.POINTER(_CShard)
+        lib.pact_adamw_commit.argtypes = [P, ctypes.c_uint64, ctypes.POINTER(_CHyper)]
+        lib.pact_adamw_commit.restype = ctypes.c_int
+        lib.pact_shard_digest.argtypes = [P]
+        lib.pact_shard_digest.restype = ctypes.c_int
+        lib.pact_bf16_digest.argtypes = [P, ctypes.c_void_p]
+        lib.pact_bf16_digest.restype = ctypes.c_int
+        lib.pact_digest_slots.argtypes = [P]
+        lib.pact_digest_slots.restype = ctypes.c_int64
+        lib.pact_stream_probe.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_uint64, ctypes.c_void_p]
+        lib.pact_stream_probe.restype = ctypes.c_int
+        lib.pact_strerror.argtypes = [ctypes.c_int]
+        lib.pact_strerror.restype = ctypes.c_char_p
+        lib.pact_last_hip_error.argtypes = []
+        lib.pact_last_hip_error.restype = ctypes.c_int
+        lib.pact_version.argtypes = []
+        lib.pact_version.restype = ctypes.c_int
+        _LIB = lib
+    return _LIB
+
+
+def _strerror(code: int) -> str:
+    return _lib().pact_strerror(code).decode()
+
+
+@dataclass(frozen=True)
+class Hyper:
+    """AdamW hyperparameters (rounded to binary32 by the library's ABI)."""
+
+    lr: float = 3e-4
+    beta1: float = 0.9
+    beta2: float = 0.95
+    eps: float = 1e-8
+    weight_decay: float = 0.1
+
+    def _c(self) -> _CHyper:
+        return _CHyper(self.lr, self.beta1, self.beta2, self.eps, self.weight_decay)
+
+
+def _dev_tensor(t: Optional[torch.Tensor], dtype, name: str, n: int):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.dtype not in dtype:
+        raise TypeError(f"{name} must be a torch tensor of {dtype}")
+    if t.device.type != "cuda":
+        raise TypeError(f"{name} must live on a GPU (got {t.device}); there is no CPU path")
+    if not t.is_contiguous() or t.numel() != n:
+        raise ValueError(f"{name} must be contiguous with {n} elements")
+    return t
+
+
+class Shard:
+    """One rank's flat shard: fp32 param/grad/exp_avg/exp_avg_sq, a bf16 copy,
+    and the device slots the digests land in.
+
+    ``segments``: optional [(offset, length, hyper_index)] in shard elements
+    with ``hypers`` the per-segment table; without it the shard is one segment.
+    """
+
+    def __init__(self, param: torch.Tensor, grad: Optional[torch.Tensor], exp_avg: torch.Tensor,
+                 exp_avg_sq: torch.Tensor, param_bf16: Optional[torch.Tensor], global_offset: int = 0,
+                 segments: Optional[Sequence[Tuple[int, int, int]]] = None,
+                 hypers: Optional[Sequence[Hyper]] = None):
+        n = param.numel()
+        f32 = (torch.float32,)
+        self.param = _dev_tensor(param, f32, "param", n)
+        self.grad = _dev_tensor(grad, f32, "grad", n)
+        self.exp_avg = _dev_tensor(exp_avg, f32, "exp_avg", n)
+        self.exp_avg_sq = _dev_tensor(exp_avg_sq, f32, "exp_avg_sq", n)
+        self.param_bf16 = _dev_tensor(param_bf16, (torch.bfloat16, torch.int16), "param_bf16", n)
+        self.numel = n
+        self.global_offset = int(global_offset)
+        self.device = param.device
+        self.segments = None if segments is None else [tuple(int(x) for x in s) for s in segments]
+        self.hypers = None if hypers is None else list(hypers)
+        if self.segments is not None and not self.hypers:
+            raise ValueError("a segment table needs a hyper table")
+        self.slots = 1 if self.segments is None else len(self.segments) + 1
+        self.digest = torch.zeros(self.slots, dtype=torch.int64, device=self.device)
+        # the C segment and hyper tables are built once and kept alive here
+        if self.segments is not None:
+            self._csegs = (_CSegment * len(self.segments))(*[_CSegment(o, l, h, 0) for o, l, h in self.segments])
+            self._chypers = (_CHyper * len(self.hypers))(*[h._c() for h in self.hypers])
+        else:
+            self._csegs = None
+            self._chypers = None
+
+    def _c(self, digest_out: Optional[torch.Tensor] = None) -> _CShard:
+        def ptr(t):
+            return None if t is None else t.data_ptr()
+
+        s = _CShard()
+        s.param, s.grad = ptr(self.param), ptr(self.grad)
+        s.exp_avg, s.exp_avg_sq, s.param_bf16 = ptr(self.exp_avg), ptr(self.exp_avg_sq), ptr(self.param_bf16)
+        s.numel, s.global_offset = self.numel, self.global_offset
+        if self._csegs is not None:
+            s.segs = ctypes.cast(self._csegs, ctypes.POINTER(_CSegment))
+            s.num_segs = len(self.segments)
+            s.hypers = ctypes.cast(self._chypers, ctypes.POINTER(_CHyper))
+            s.num_hypers = len(self.hypers)
+        s.digest_dev = (digest_out if digest_out is not None else self.digest).data_ptr()
+        s.stream = torch.cuda.current_stream(self.device).cuda_stream
+        return s
+
+
+def _call(what: str, rc: int) -> None:
+    if rc != PACT_OK:
+        raise PactError(rc, what)
+
+
+def digest_slots(shard: Shard) -> int:
+    return int(_lib().pact_digest_slots(ctypes.byref(shard._c())))
+
+
+def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None) -> torch.Tensor:
+    """Commit one AdamW step on the shard (in place) and digest the result.
+
+    Returns the device tensor of digest slots (int64 holding uint64 bits); it
+    holds the values once the current stream reaches this point.
+    """
+    if shard.segments is None and hyper is None:
+        hyper = Hyper()
+    ch = hyper._c() if hyper is not None else None
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_adamw_commit(ctypes.byref(shard._c()), int(step),
+                                      ctypes.byref(ch) if ch is not None else None)
+    _call("pact_adamw_commit", rc)
+    return shard.digest
+
+
+def shard_digest(shard: Shard) -> torch.Tensor:
+    """Digest of the shard's current (param, exp_avg, exp_avg_sq)."""
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_shard_digest(ctypes.byref(shard._c()))
+    _call("pact_shard_digest", rc)
+    return shard.digest
+
+
+def bf16_digest(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Digest (tag 3) of the bf16 copy, into ``out`` (allocated if None)."""
+    if out is None:
+        out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_bf16_digest(ctypes.byref(shard._c()), out.data_ptr())
+    _call("pact_bf16_digest", rc)
+    return out
+
+
+def stream_probe(i0, i1, i2, i3, o0, o2, o3, oh) -> None:
+    """30-byte/element streaming probe (measurement support)."""
+    n = i0.numel()
+    with torch.cuda.device(i0.device):
+        rc = _lib().pact_stream_probe(i0.data_ptr(), i1.data_ptr(), i2.data_ptr(), i3.data_ptr(),
+                                      o0.data_ptr(), o2.data_ptr(), o3.data_ptr(), oh.data_ptr(), n,
+                                      torch.cuda.current_stream(i0.device).cuda_stream)
+    _call("pact_stream_probe", rc)
+
+
+def to_u64(t: torch.Tensor):
+    """Digest slots as Python ints (uint64); synchronizes with the device."""
+    return [int(x) & MASK64 for x in t.cpu().tolist()]

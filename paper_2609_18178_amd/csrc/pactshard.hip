@@ -1,0 +1,330 @@
+// pactshard.hip -- host side of libpactshard: argument validation, the
+// per-step scalars, the segment batching and the launches.  The C ABI and
+// its contract are in include/pactshard.h.
+#include "pactshard.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "launch.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr uint64_t kIndexLimit = 1ull << 56;  // indices must stay below the tag bits
+
+int fail_hip(hipError_t e) {
+    g_last_hip_error = static_cast<int>(e);
+    return PACT_EHIP;
+}
+
+// ---------------------------------------------------------------------------
+// launch geometry: persistent workgroups per compute unit, per device
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
+constexpr uint32_t kGroupsPerCu = 8;
+
+int g_cus[kMaxDevices];
+std::once_flag g_cu_once[kMaxDevices];
+
+int cu_count(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return 256;
+    std::call_once(g_cu_once[dev], [dev] {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+            n = 256;
+        }
+        g_cus[dev] = n;
+    });
+    return g_cus[dev];
+}
+
+// ---------------------------------------------------------------------------
+// validation
+// ---------------------------------------------------------------------------
+bool finite(float x) { return std::isfinite(x); }
+
+bool hyper_ok(const pact_hyper& h) {
+    return finite(h.lr) && finite(h.beta1) && finite(h.beta2) && finite(h.eps) && finite(h.weight_decay) &&
+           h.lr >= 0.0f && h.beta1 >= 0.0f && h.beta1 < 1.0f && h.beta2 >= 0.0f && h.beta2 < 1.0f &&
+           h.eps > 0.0f && h.weight_decay >= 0.0f;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+struct Span {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+bool overlaps(const std::vector<Span>& spans) {
+    for (size_t i = 0; i < spans.size(); ++i) {
+        for (size_t j = i + 1; j < spans.size(); ++j) {
+            if (spans[i].lo < spans[j].hi && spans[j].lo < spans[i].hi) return true;
+        }
+    }
+    return false;
+}
+
+// Which arrays a mode touches.
+struct Uses {
+    bool p, g, m, v, b;
+};
+
+// Checks the shard for a mode; `out` is the digest destination.  Returns 0 or
+// a PACT_E* code.  Reads no device memory and makes no HIP call.
+int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t* nslots) {
+    if (s == nullptr || out == nullptr) return PACT_EINVAL;
+    const uint64_t n = s->numel;
+    if (n > 0) {
+        if ((use.p && !s->param) || (use.g && !s->grad) || (use.m && !s->exp_avg) ||
+            (use.v && !s->exp_avg_sq) || (use.b && !s->param_bf16)) {
+            return PACT_EINVAL;
+        }
+    }
+    if (s->global_offset >= kIndexLimit || n > kIndexLimit - s->global_offset) return PACT_ERANGE;
+    if (n > (UINT64_MAX / 4)) return PACT_ERANGE;
+    if (s->segs != nullptr) {
+        if (s->num_segs == 0 || s->num_segs > 0x7FFFFFFFu) return PACT_EINVAL;
+        uint64_t prev_end = 0;
+        for (uint32_t k = 0; k < s->num_segs; ++k) {
+            const pact_segment& sg = s->segs[k];
+            if (sg.reserved != 0 || sg.offset < prev_end || sg.length > n || sg.offset > n - sg.length) {
+                return PACT_EINVAL;
+            }
+            prev_end = sg.offset + sg.length;
+        }
+    }
+    if (!aligned(out, 8)) return PACT_EALIGN;
+    if ((use.p && !aligned(s->param, 4)) || (use.g && !aligned(s->grad, 4)) || (use.m && !aligned(s->exp_avg, 4)) ||
+        (use.v && !aligned(s->exp_avg_sq, 4)) || (use.b && !aligned(s->param_bf16, 2))) {
+        return PACT_EALIGN;
+    }
+    const uint64_t slots = s->segs ? (uint64_t)s->num_segs + 1 : 1;
+    std::vector<Span> spans;
+    auto add = [&](const void* ptr, uint64_t bytes) {
+        if (ptr && bytes) {
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+            spans.push_back({lo, lo + bytes});
+        }
+    };
+    if (use.p) add(s->param, n * 4);
+    if (use.g) add(s->grad, n * 4);
+    if (use.m) add(s->exp_avg, n * 4);
+    if (use.v) add(s->exp_avg_sq, n * 4);
+    if (use.b) add(s->param_bf16, n * 2);
+    add(out, slots * 8);
+    for (const Span& sp : spans) {
+        if (sp.hi < sp.lo) return PACT_ERANGE;  // wraps the address space
+    }
+    if (overlaps(spans)) return PACT_EOVERLAP;
+    *nslots = slots;
+    return PACT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// per-step scalars: beta^t by t double multiplications from 1 (stopping once
+// neither product changes), the derived values in double, one binary32
+// rounding each
+// ---------------------------------------------------------------------------
+pact::StepScalars step_scalars(const pact_hyper& h, uint64_t t) {
+    const double beta1 = h.beta1, beta2 = h.beta2;
+    double pow1 = 1.0, pow2 = 1.0;
+    for (uint64_t k = 0; k < t; ++k) {
+        const double next1 = pow1 * beta1;
+        const double next2 = pow2 * beta2;
+        const bool fixed = next1 == pow1 && next2 == pow2;
+        pow1 = next1;
+        pow2 = next2;
+        if (fixed) break;
+    }
+    const double lr = h.lr, wd = h.weight_decay;
+    pact::StepScalars sc;
+    sc.beta1 = h.beta1;
+    sc.beta2 = h.beta2;
+    sc.eps = h.eps;
+    sc.decay = static_cast<float>(1.0 - lr * wd);
+    sc.omb1 = static_cast<float>(1.0 - beta1);
+    sc.omb2 = static_cast<float>(1.0 - beta2);
+    sc.step_size = static_cast<float>(lr / (1.0 - pow1));
+    sc.rs_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - pow2));
+    return sc;
+}
+
+// ---------------------------------------------------------------------------
+// enqueue one mode over the shard's segments
+// ---------------------------------------------------------------------------
+struct SegWork {
+    uint64_t first, count;
+    pact::StepScalars sc;
+};
+
+int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots) {
+    hipStream_t stream = static_cast<hipStream_t>(s->stream);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e);
+    const uint32_t max_grid = (uint32_t)cu_count(dev) * kGroupsPerCu;
+
+    e = pact::launch_zero(out, (uint32_t)nslots, stream);
+    if (e != hipSuccess) return fail_hip(e);
+
+    pact::Arrays a;
+    a.p = s->param;
+    a.g = s->grad;
+    a.m = s->exp_avg;
+    a.v = s->exp_avg_sq;
+    a.b = s->param_bf16;
+    a.goff = s->global_offset;
+    a.digest = out;
+
+    const bool per_segment = s->segs != nullptr;
+    const uint32_t total_slot = (uint32_t)(nslots - 1);
+    for (size_t first = 0; first < work.size(); first += pact::kSegsPerLaunch) {
+        const size_t cnt = std::min<size_t>(pact::kSegsPerLaunch, work.size() - first);
+        pact::Batch b;
+        std::memset(&b, 0, sizeof b);
+        b.nseg = (uint32_t)cnt;
+        b.slot0 = (uint32_t)first;
+        b.total_slot = total_slot;
+        b.per_segment = per_segment ? 1u : 0u;
+        uint64_t tiles = 0;
+        for (size_t k = 0; k < cnt; ++k) {
+            const SegWork& w = work[first + k];
+            b.tile_begin[k] = tiles;
+            tiles += (w.count + pact::kTile - 1) / pact::kTile;
+            b.elem_begin[k] = w.first;
+            b.elem_count[k] = w.count;
+            b.sc[k] = w.sc;
+            bool ok = true;
+            if (mode != pact::Mode::Bf16Digest) {
+                ok = aligned(a.p + w.first, 16) && aligned(a.m + w.first, 16) && aligned(a.v + w.first, 16);
+                if (mode == pact::Mode::Commit) {
+                    ok = ok && aligned(a.g + w.first, 16) && aligned(a.b + w.first, 8);
+                }
+            } else {
+                ok = aligned(a.b + w.first, 8);
+            }
+            b.vec_ok[k] = ok ? 1u : 0u;
+        }
+        b.tile_begin[cnt] = tiles;
+        if (tiles == 0) continue;
+        const uint32_t grid = (uint32_t)std::min<uint64_t>(tiles, max_grid);
+        e = pact::launch_batch(mode, a, b, grid, stream);
+        if (e != hipSuccess) return fail_hip(e);
+    }
+    return PACT_OK;
+}
+
+std::vector<SegWork> segment_work(const pact_shard* s, const pact_hyper* single, uint64_t step, bool need_hyper,
+                                  int* err) {
+    std::vector<SegWork> work;
+    *err = PACT_OK;
+    if (s->segs == nullptr) {
+        SegWork w{0, s->numel, {}};
+        if (need_hyper) w.sc = step_scalars(*single, step);
+        if (s->numel > 0) work.push_back(w);
+        return work;
+    }
+    if (need_hyper && s->hypers == nullptr) {
+        *err = PACT_EINVAL;
+        return work;
+    }
+    work.reserve(s->num_segs);
+    for (uint32_t k = 0; k < s->num_segs; ++k) {
+        const pact_segment& sg = s->segs[k];
+        SegWork w{sg.offset, sg.length, {}};
+        if (need_hyper) {
+            if (sg.hyper_index >= s->num_hypers || !hyper_ok(s->hypers[sg.hyper_index])) {
+                *err = PACT_EINVAL;
+                return {};
+            }
+            w.sc = step_scalars(s->hypers[sg.hyper_index], step);
+        }
+        work.push_back(w);  // empty segments keep their slot (digest 0)
+    }
+    return work;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t pact_digest_slots(const pact_shard* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    return s->segs ? (int64_t)s->num_segs + 1 : 1;
+}
+
+int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
+    if (s == nullptr || step == 0) return PACT_EINVAL;
+    if (s->segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
+    uint64_t nslots = 0;
+    int rc = validate(s, Uses{true, true, true, true, true}, s->digest_dev, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(pact::Mode::Commit, s, work, s->digest_dev, nslots);
+}
+
+int pact_shard_digest(const pact_shard* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    uint64_t nslots = 0;
+    int rc = validate(s, Uses{true, false, true, true, false}, s->digest_dev, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(pact::Mode::StateDigest, s, work, s->digest_dev, nslots);
+}
+
+int pact_bf16_digest(const pact_shard* s, uint64_t* dev_out) {
+    if (s == nullptr) return PACT_EINVAL;
+    uint64_t nslots = 0;
+    int rc = validate(s, Uses{false, false, false, false, true}, dev_out, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(pact::Mode::Bf16Digest, s, work, dev_out, nslots);
+}
+
+int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
+                      float* out2, float* out3, uint16_t* out_half, uint64_t n, void* stream) {
+    if (n == 0) return PACT_OK;
+    if (!in0 || !in1 || !in2 || !in3 || !out0 || !out2 || !out3 || !out_half || (n % pact::kVec) != 0) {
+        return PACT_EINVAL;
+    }
+    if (!aligned(in0, 16) || !aligned(in1, 16) || !aligned(in2, 16) || !aligned(in3, 16) || !aligned(out0, 16) ||
+        !aligned(out2, 16) || !aligned(out3, 16) || !aligned(out_half, 8)) {
+        return PACT_EALIGN;
+    }
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e);
+    const uint64_t nvec = n / pact::kVec;
+    const uint64_t groups = (nvec + pact::kBlock - 1) / pact::kBlock;
+    const uint32_t grid = (uint32_t)std::min<uint64_t>(groups, (uint64_t)cu_count(dev) * kGroupsPerCu);
+    e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n, grid,
+                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail_hip(e);
+    return PACT_OK;
+}
+
+const char* pact_strerror(int code) {
+    switch (code) {
+        case PACT_OK: return "ok";
+        case PACT_EINVAL: return "invalid argument";
+        case PACT_EALIGN: return "misaligned pointer";
+        case PACT_EOVERLAP: return "buffers overlap";
+        case PACT_ERANGE: return "index range reaches the digest tag bits (2^56) or wraps";
+        case PACT_EHIP: return "HIP call failed";
+        default: return "unknown error";
+    }
+}
+
+int pact_last_hip_error(void) { return g_last_hip_error; }
+
+int pact_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,356 @@
+"""GPU path vs the CPU oracle, element by element, through the C ABI.
+
+The library is built in exact mode (no contraction, IEEE sqrt/div, fp32
+denormals kept), so the contract is bit-exact for every output: p', m', v',
+the bf16 copy and every digest slot.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.helpers import (M64, assert_bitwise, host, make_shard, o_hyper, g_hyper, oracle_commit_parallel,
+                           oracle_digest_parallel)
+
+pytestmark = pytest.mark.gpu
+
+H = wl.DEFAULT_HYPER
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_18178_amd as pk
+
+    pk._lib()
+    yield
+
+
+def _pk():
+    import paper_2609_18178_amd as pk
+
+    return pk
+
+
+def _compare_full(sh, p, m, v, b, what=""):
+    assert_bitwise(what + "param", host(sh.param), p)
+    assert_bitwise(what + "exp_avg", host(sh.exp_avg), m)
+    assert_bitwise(what + "exp_avg_sq", host(sh.exp_avg_sq), v)
+    assert_bitwise(what + "bf16", host(sh.param_bf16).view(np.uint16), b)
+
+
+def _commit_both(w, start=0, count=None, hyper=H, step=None):
+    """Inputs of workload w (slice), committed on the GPU and by the oracle."""
+    pk = _pk()
+    p, g, m, v = wl.arrays_host(w, start, count)
+    sh = make_shard(p, g, m, v, w.global_offset + start)
+    step = step or w.first_step
+    d_gpu = pk.to_u64(pk.adamw_commit(sh, step, g_hyper(hyper)))[0]
+    b = np.zeros(p.size, np.uint16)
+    d_ref = oracle_commit_parallel(p, g, m, v, b, o_hyper(hyper), step, w.global_offset + start)
+    return sh, (p, g, m, v, b), d_gpu, d_ref
+
+
+def test_tiny_full_parity():
+    """1,048,576 elements, step 1 from m = v = 0: every output bitwise."""
+    pk = _pk()
+    w = wl.WORKLOADS["tiny"]
+    sh, (p, g, m, v, b), d_gpu, d_ref = _commit_both(w)
+    assert d_gpu == d_ref
+    _compare_full(sh, p, m, v, b)
+    # the standalone digest of the committed state equals the fused one
+    assert pk.to_u64(pk.shard_digest(sh))[0] == d_ref
+    assert pk.to_u64(pk.bf16_digest(sh))[0] == oracle.bf16_digest(b, w.global_offset)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 63, 64, 65, 2047, 2048, 2049, 4093, 10007, 100003])
+@pytest.mark.parametrize("shift", [0, 1, 2, 3])
+def test_ragged_and_unaligned(n, shift):
+    """Ragged tails and views starting 1-3 elements past a 16-byte boundary
+    (element-wise path) give the oracle's bits."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    full = [torch.zeros(n + 8, dtype=torch.float32, device="cuda") for _ in range(4)]
+    views = []
+    for t, a in zip(full, (p, g, m, v)):
+        t[shift:shift + n] = torch.from_numpy(a).cuda()
+        views.append(t[shift:shift + n])
+    bfull = torch.zeros(n + 8, dtype=torch.int16, device="cuda")
+    sh = pk.Shard(*views, bfull[shift:shift + n], global_offset=w.global_offset)
+    d_gpu = pk.to_u64(pk.adamw_commit(sh, 100, g_hyper(H)))[0]
+    b = np.zeros(n, np.uint16)
+    d_ref = oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), 100, w.global_offset)
+    assert d_gpu == d_ref
+    _compare_full(sh, p, m, v, b)
+    # guard elements around the view are untouched
+    for t in full + [bfull]:
+        h = host(t)
+        assert not h[:shift].any() and not h[shift + n:].any()
+
+
+def test_empty_shard():
+    """n = 0: the digest is 0 and nothing is read or written."""
+    import torch
+
+    pk = _pk()
+    e = torch.zeros(0, dtype=torch.float32, device="cuda")
+    sh = pk.Shard(e, e.clone(), e.clone(), e.clone(), torch.zeros(0, dtype=torch.int16, device="cuda"), 5)
+    sh.digest.fill_(123)
+    assert pk.to_u64(pk.adamw_commit(sh, 1, g_hyper(H))) == [0]
+    sh.digest.fill_(7)
+    assert pk.to_u64(pk.shard_digest(sh)) == [0]
+
+
+def test_decoder1b_shard_ten_commits():
+    """76,000,000-element shard (rank 15 of a 1.216B decoder at 16 ranks), warm
+    state from step 100, ten commits with a fresh gradient each: every per-step
+    digest and, at the end, every output bitwise."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    p, g, m, v = wl.arrays_host(w)
+    sh = make_shard(p, g, m, v, w.global_offset)
+    b = np.zeros(p.size, np.uint16)
+    for step in range(w.first_step, w.first_step + w.commits):
+        if step != w.first_step:
+            g = wl.grad_host(w, step)
+            sh.grad.copy_(torch.from_numpy(g))
+        d_gpu = pk.to_u64(pk.adamw_commit(sh, step, g_hyper(H)))[0]
+        d_ref = oracle_commit_parallel(p, g, m, v, b, o_hyper(H), step, w.global_offset)
+        assert d_gpu == d_ref, f"step {step}"
+    _compare_full(sh, p, m, v, b)
+
+
+def test_repeated_sequences_are_bit_identical():
+    """Ten repetitions of a ten-commit sequence give identical digest vectors
+    (the ten-repair bitwise check of Sec. IV-G, as digests), equal to the
+    oracle's vector."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    n = 1 << 22
+    p0, g0, m0, v0 = wl.arrays_host(w, 0, n)
+    grads = [wl.grad_host(w, s, 0, n) for s in range(100, 110)]
+    vectors = []
+    for rep in range(10):
+        sh = make_shard(p0, g0, m0, v0, w.global_offset)
+        vec = []
+        for k, step in enumerate(range(100, 110)):
+            sh.grad.copy_(torch.from_numpy(grads[k]))
+            vec.append(pk.to_u64(pk.adamw_commit(sh, step, g_hyper(H)))[0])
+        vectors.append(vec)
+    assert all(vec == vectors[0] for vec in vectors)
+    p, m, v = p0.copy(), m0.copy(), v0.copy()
+    b = np.zeros(n, np.uint16)
+    ref = [oracle.commit_and_digest(p, grads[k], m, v, b, o_hyper(H), 100 + k, w.global_offset) for k in range(10)]
+    assert vectors[0] == ref
+
+
+@pytest.mark.parametrize("goff", [2 ** 32 - 1000, 2 ** 56 - 5001])
+def test_global_index_edges(goff):
+    """Indices crossing 2^32, and the last indices below the tag bits."""
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    n = 5001
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    sh = make_shard(p, g, m, v, goff)
+    d_gpu = pk.to_u64(pk.adamw_commit(sh, 3, g_hyper(H)))[0]
+    b = np.zeros(n, np.uint16)
+    assert d_gpu == oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), 3, goff)
+    _compare_full(sh, p, m, v, b)
+    sh.global_offset = 2 ** 56 - n + 1
+    with pytest.raises(pk.PactError) as e:
+        pk.adamw_commit(sh, 4, g_hyper(H))
+    assert e.value.code == pk.PACT_ERANGE
+
+
+def test_multi_segment_shrunken_mistral():
+    """Real Mistral tensor roles at a small size with padding, four hyper
+    sets (norms without decay, lm_head with its own beta2): per-segment
+    digests, their sum, every output, and untouched padding."""
+    import torch
+
+    pk = _pk()
+    w = wl.shrunken_mistral()
+    p, g, m, v = wl.arrays_host(w)
+    sh = make_shard(p, g, m, v, w.global_offset, segments=w.segments, hypers=w.hypers)
+    sh.param_bf16.fill_(0x5A5A)
+    got = pk.to_u64(pk.adamw_commit(sh, 5))
+    b = np.full(p.size, 0x5A5A, np.uint16)
+    per, total = oracle.commit_segments(p, g, m, v, b, w.segments, [o_hyper(h) for h in w.hypers], 5,
+                                        w.global_offset)
+    assert got == per + [total]
+    _compare_full(sh, p, m, v, b)
+    assert pk.to_u64(pk.shard_digest(sh)) == per + [total]
+    bd = pk.to_u64(pk.bf16_digest(sh))
+    want = [oracle.bf16_digest(b[o:o + ln], w.global_offset + o) for o, ln, _ in w.segments]
+    assert bd == want + [sum(want) & M64]
+    del torch
+
+
+def test_many_segments_span_several_launches():
+    """More segments than one launch carries (32), with empty, one-element,
+    unaligned and ragged segments and gaps between them."""
+    pk = _pk()
+    rng = np.random.default_rng(21)
+    segs, off = [], 3
+    for k in range(100):
+        ln = int(rng.choice([0, 1, 5, 2048, 3001, 4096, 9999]))
+        segs.append((off, ln, k % 3))
+        off += ln + int(rng.integers(0, 9))
+    n = off + 17
+    hypers = [H, dict(H, weight_decay=0.0), dict(H, lr=1e-3, beta2=0.99)]
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    sh = make_shard(p, g, m, v, 777, segments=segs, hypers=hypers)
+    got = pk.to_u64(pk.adamw_commit(sh, 9))
+    b = np.zeros(n, np.uint16)
+    per, total = oracle.commit_segments(p, g, m, v, b, segs, [o_hyper(h) for h in hypers], 9, 777)
+    assert got == per + [total]
+    _compare_full(sh, p, m, v, b)
+
+
+def test_special_values_lr_zero_keeps_every_pattern():
+    """lr = 0, g = 0, m = v = 0: p' == p for every non-NaN binary32 pattern
+    (denormals, -0, infinities), so the bf16 copy is the RNE of each pattern:
+    all 65,536 upper halves crossed with the rounding-boundary lower halves."""
+    import torch
+
+    pk = _pk()
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF, 0x1234, 0xC000], dtype=np.uint32)
+    pat = (hi[:, None] | lows[None, :]).reshape(-1)
+    pat = pat[(pat & 0x7FFFFFFF) <= 0x7F800000]
+    n = pat.size
+    p = pat.view(np.float32).copy()
+    z = np.zeros(n, np.float32)
+    sh = make_shard(p, z, z, z, 0)
+    pk.adamw_commit(sh, 1, pk.Hyper(lr=0.0, weight_decay=0.0))
+    assert_bitwise("param", host(sh.param), p)
+    assert_bitwise("bf16", host(sh.param_bf16).view(np.uint16), oracle.bf16_rne_bits(pat))
+    b = np.zeros(n, np.uint16)
+    pp, mm, vv = p.copy(), z.copy(), z.copy()
+    d = oracle.commit_and_digest(pp, z.copy(), mm, vv, b, oracle.Hyper(lr=0.0, weight_decay=0.0), 1, 0)
+    assert pk.to_u64(sh.digest)[0] == d
+    del torch
+
+
+def test_denormal_state_is_kept():
+    """Denormal moments and weights go through the update without flushing."""
+    pk = _pk()
+    rng = np.random.default_rng(4)
+    n = 65536
+    p = (rng.standard_normal(n) * 1e-39).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-40).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-41).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 1e-42).astype(np.float32)
+    hy = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-30, weight_decay=0.01)
+    sh = make_shard(p, g, m, v, 0)
+    assert ((m.view(np.uint32) & 0x7F800000) == 0).all()  # every input moment is denormal or 0
+    d = pk.to_u64(pk.adamw_commit(sh, 2, g_hyper(hy)))[0]
+    b = np.zeros(n, np.uint16)
+    assert d == oracle.commit_and_digest(p, g, m, v, b, o_hyper(hy), 2, 0)
+    _compare_full(sh, p, m, v, b)
+    assert ((m.view(np.uint32) & 0x7F800000) == 0).sum() > n // 2  # and so are most outputs
+
+
+def test_shard_digest_of_arbitrary_bits():
+    """shard_digest is integer work only: any bit patterns, NaNs included."""
+    import torch
+
+    pk = _pk()
+    rng = np.random.default_rng(6)
+    n = 300001
+    arr = [rng.integers(0, 2 ** 32, n, dtype=np.uint64).astype(np.uint32).view(np.float32) for _ in range(3)]
+    t = [torch.from_numpy(a.copy()).cuda() for a in arr]
+    sh = pk.Shard(t[0], None, t[1], t[2], None, global_offset=123456789)
+    assert pk.to_u64(pk.shard_digest(sh))[0] == oracle.state_digest(*arr, 123456789)
+
+
+def test_digest_composes_over_sub_shards():
+    """Digests of sub-shard views (with their own offsets) sum to the digest
+    of the whole, on the GPU."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    n = 1_000_003
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    tp, tm, tv = (torch.from_numpy(a).cuda() for a in (p, m, v))
+    whole = pk.to_u64(pk.shard_digest(pk.Shard(tp, None, tm, tv, None, 99)))[0]
+    cuts = [0, 1, 4097, 500000, 999999, n]
+    s = 0
+    for a, z in zip(cuts[:-1], cuts[1:]):
+        s += pk.to_u64(pk.shard_digest(pk.Shard(tp[a:z], None, tm[a:z], tv[a:z], None, 99 + a)))[0]
+    assert s & M64 == whole == oracle.state_digest(p, m, v, 99)
+
+
+def test_state_breaks_are_detected():
+    """A commit applied to only part of the shard gives a digest different
+    from both the frontier before and after; applying a commit twice differs
+    from applying it once."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    n = 1 << 20
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    before = oracle.state_digest(p, m, v, w.global_offset)
+    full = make_shard(p, g, m, v, w.global_offset)
+    after = pk.to_u64(pk.adamw_commit(full, 100, g_hyper(H)))[0]
+    half = make_shard(p, g, m, v, w.global_offset)
+    hv = pk.Shard(half.param[: n // 2], half.grad[: n // 2], half.exp_avg[: n // 2], half.exp_avg_sq[: n // 2],
+                  half.param_bf16[: n // 2], w.global_offset)
+    pk.adamw_commit(hv, 100, g_hyper(H))
+    torn = pk.to_u64(pk.shard_digest(half))[0]
+    assert len({before, after, torn}) == 3
+    twice = pk.to_u64(pk.adamw_commit(full, 100, g_hyper(H)))[0]
+    assert twice != after
+    del torch
+
+
+def test_stream_probe_moves_the_bytes():
+    import torch
+
+    pk = _pk()
+    n = 1 << 20
+    a, b_, c, d = (torch.randn(n, device="cuda") for _ in range(4))
+    ref = [(a + b_).clone(), c.clone(), d.clone()]
+    h = torch.zeros(n, dtype=torch.int16, device="cuda")
+    pk.stream_probe(a, b_, c, d, a, c, d, h)
+    assert torch.equal(a, ref[0]) and torch.equal(c, ref[1]) and torch.equal(d, ref[2])
+    top = (ref[0].view(torch.int32) >> 16).to(torch.int16)
+    assert torch.equal(h, top)
+
+
+@pytest.mark.slow
+def test_mistral7b_shard16_full_size():
+    """The benchmark workload at full size and in the benchmark's launch
+    configuration: the 453,001,472-element 1/16 shard of Mistral-7B at rank
+    15 (indices beyond 2^32), warm state at step 5.  Digest and bf16 digest
+    against the oracle over host threads, and every output bitwise."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    print(f"[{w.name}] drawing {w.numel} elements", flush=True)
+    p, g, m, v = wl.arrays_host(w)
+    sh = make_shard(p, g, m, v, w.global_offset)
+    print(f"[{w.name}] GPU commit", flush=True)
+    d_gpu = pk.to_u64(pk.adamw_commit(sh, w.first_step, g_hyper(H)))[0]
+    bd_gpu = pk.to_u64(pk.bf16_digest(sh))[0]
+    print(f"[{w.name}] oracle commit", flush=True)
+    b = np.zeros(p.size, np.uint16)
+    d_ref = oracle_commit_parallel(p, g, m, v, b, o_hyper(H), w.first_step, w.global_offset)
+    assert d_gpu == d_ref
+    assert bd_gpu == oracle.bf16_digest(b, w.global_offset)
+    _compare_full(sh, p, m, v, b)
+    assert pk.to_u64(pk.shard_digest(sh))[0] == oracle_digest_parallel(p, m, v, w.global_offset)
+    del torch
