@@ -17,7 +17,6 @@ import argparse
 import hashlib
 import json
 import os
-import platform
 import sys
 import time
 
@@ -98,7 +97,7 @@ def cpu_baseline(w, seconds: float) -> dict:
                   f"commit+digest repeated for >= {seconds:g} s per leg; the oracle cut into {threads} slices "
                   f"run by {threads} threads",
         "single_thread_value": single,
-        "cpu_model": platform.processor() or _cpu_model(),
+        "cpu_model": _cpu_model(),
     }
 
 

@@ -15,12 +15,14 @@
 // Wrapping addition is associative and commutative, so the order in which
 // workgroups arrive cannot change the result.
 //
-// Arithmetic is the library contract in pactshard.h: every binary32
-// operation is written with an explicit round-to-nearest intrinsic so no
-// operation can be contracted or reassociated; sqrt and division are the
-// IEEE-correct forms.  The translation unit is built with
-// -ffp-contract=off and fp32 denormals kept.
+// Arithmetic is the library contract in pactshard.h: one IEEE binary32
+// rounding per operation, no contraction or reassociation (the translation
+// unit is built with -ffp-contract=off and without fast-math), correctly
+// rounded sqrt and division, fp32 denormals kept.
 #include "launch.h"
+
+// No fused multiply-add anywhere in this file, whatever the command line says.
+#pragma clang fp contract(off)
 
 namespace pact {
 namespace {
@@ -43,15 +45,28 @@ __device__ __forceinline__ uint64_t hash_word(uint32_t word, uint64_t tagged_ind
 }
 
 // ---------------------------------------------------------------------------
-// AdamW on one element (contract order; one rounding per operation)
+// AdamW on one element, in the contract's order.  With -ffp-contract=off and
+// no fast-math flags every +, -, * below is one IEEE binary32 operation
+// rounded to nearest even, '/' is the correctly rounded division, and
+// __builtin_sqrtf is lowered to the correctly rounded square root (the
+// -fhip-fp32-correctly-rounded-divide-sqrt default).  HIP's __fsqrt_rn is
+// NOT used: unless OCML_BASIC_ROUNDED_OPERATIONS is defined it maps to the
+// hardware's approximate v_sqrt_f32.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void adamw(float& p, float g, float& m, float& v, const StepScalars& s) {
-    const float p_dec = __fmul_rn(p, s.decay);
-    const float m_new = __fadd_rn(__fmul_rn(s.beta1, m), __fmul_rn(s.omb1, g));
-    const float v_new = __fadd_rn(__fmul_rn(s.beta2, v), __fmul_rn(s.omb2, __fmul_rn(g, g)));
-    const float den = __fadd_rn(__fmul_rn(__fsqrt_rn(v_new), s.rs_bc2), s.eps);
-    const float step = __fmul_rn(s.step_size, __fdiv_rn(m_new, den));
-    p = __fsub_rn(p_dec, step);
+    const float p_dec = p * s.decay;
+    const float m_keep = s.beta1 * m;
+    const float m_push = s.omb1 * g;
+    const float m_new = m_keep + m_push;
+    const float g_sq = g * g;
+    const float v_keep = s.beta2 * v;
+    const float v_push = s.omb2 * g_sq;
+    const float v_new = v_keep + v_push;
+    const float root = __builtin_sqrtf(v_new);
+    const float den = root * s.rs_bc2 + s.eps;
+    const float ratio = m_new / den;
+    const float step = s.step_size * ratio;
+    p = p_dec - step;
     m = m_new;
     v = v_new;
 }
