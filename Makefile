@@ -36,7 +36,14 @@ workloads/libgen.so: workloads/gen.c
 $(LIB): $(LIB_SRCS) $(LIB_HDRS)
 	$(HIPCC) $(HIPFLAGS) -o $@ $(LIB_SRCS)
 
+# gfx950 assembly of the kernels, for inspection and the hazard test
+isa: _build/kernels-gfx950.s
+_build/kernels-gfx950.s: $(PKG)/csrc/kernels.hip $(LIB_HDRS)
+	mkdir -p _build
+	$(HIPCC) $(filter-out -shared -fPIC,$(HIPFLAGS)) --cuda-device-only -S -o $@ $(PKG)/csrc/kernels.hip
+
 clean:
 	rm -f $(LIB) oracle/liboracle.so workloads/libgen.so
+	rm -rf _build
 
-.PHONY: all clean
+.PHONY: all clean isa

@@ -38,13 +38,16 @@
  * aligned in the bf16 array runs the vector path, any other segment the
  * element-wise path, with identical results.
  *
- * Segments.  segs == NULL: the shard is one segment [0, numel) updated with
+ * Segments (at most 2^24).  segs == NULL: the shard is one segment [0, numel) updated with
  * *hyper, and digest_dev[0] receives D.  Otherwise segs[0..num_segs) lists
  * disjoint ranges (offset, length, hyper_index) in increasing offset order
  * inside [0, numel); elements outside every segment (padding) are neither
  * read, written nor digested; hypers[hyper_index] applies per segment and
  * `hyper` is ignored; digest_dev[0..num_segs) receive the per-segment digests
  * and digest_dev[num_segs] their sum.  pact_digest_slots() gives the count.
+ *
+ * Workspace.  Optional caller-owned device scratch for the digest's partial
+ * sums; see pact_workspace_bytes().
  *
  * Streams and completion.  Every call only enqueues work on `stream` (a
  * hipStream_t; NULL is the default stream) and returns; the digest slots
@@ -107,12 +110,25 @@ typedef struct pact_shard {
     uint32_t num_hypers;
     const pact_hyper* hypers;/* num_hypers entries when segs != NULL            */
     uint64_t* digest_dev;    /* device, pact_digest_slots() uint64 slots        */
+    void* workspace;         /* device scratch or NULL, see pact_workspace_bytes */
+    uint64_t workspace_bytes;/* size of workspace in bytes                      */
     void* stream;            /* hipStream_t                                     */
 } pact_shard;
 
 /* Number of uint64 digest slots a call on this shard writes: 1 without
  * segments, num_segs + 1 with them; negative error code if s is NULL. */
 int64_t pact_digest_slots(const pact_shard* s);
+
+/* Bytes of device workspace that lets a call spread its digest partial sums
+ * over several memory locations (16 lanes, 256 bytes apart, per digest slot)
+ * instead of funnelling one 64-bit atomic per 4096-element tile into a single
+ * address, which serializes on large shards.  The caller allocates it (8-byte
+ * aligned, disjoint from every other buffer) and may reuse it for any later
+ * call on the same stream; its contents on entry do not matter and on return
+ * are unspecified.  workspace == NULL is valid: the call is then correct but
+ * slower.  A non-NULL workspace with workspace_bytes below this figure is
+ * PACT_EINVAL.  Negative error code if s is NULL. */
+int64_t pact_workspace_bytes(const pact_shard* s);
 
 /* The fused commit (Sec. III-A: the update after which W, M, V count as
  * committed): reads p, g, m, v once, writes p', m', v' in place and the bf16

@@ -57,7 +57,8 @@ class _CShard(ctypes.Structure):
         ("exp_avg_sq", ctypes.c_void_p), ("param_bf16", ctypes.c_void_p),
         ("numel", ctypes.c_uint64), ("global_offset", ctypes.c_uint64),
         ("segs", ctypes.POINTER(_CSegment)), ("num_segs", ctypes.c_uint32), ("num_hypers", ctypes.c_uint32),
-        ("hypers", ctypes.POINTER(_CHyper)), ("digest_dev", ctypes.c_void_p), ("stream", ctypes.c_void_p),
+        ("hypers", ctypes.POINTER(_CHyper)), ("digest_dev", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_uint64), ("stream", ctypes.c_void_p),
     ]
 
 
@@ -82,6 +83,8 @@ def _lib():
         lib.pact_bf16_digest.restype = ctypes.c_int
         lib.pact_digest_slots.argtypes = [P]
         lib.pact_digest_slots.restype = ctypes.c_int64
+        lib.pact_workspace_bytes.argtypes = [P]
+        lib.pact_workspace_bytes.restype = ctypes.c_int64
         lib.pact_stream_probe.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_uint64, ctypes.c_void_p]
         lib.pact_stream_probe.restype = ctypes.c_int
         lib.pact_strerror.argtypes = [ctypes.c_int]
@@ -130,12 +133,14 @@ class Shard:
 
     ``segments``: optional [(offset, length, hyper_index)] in shard elements
     with ``hypers`` the per-segment table; without it the shard is one segment.
+    ``use_workspace``: allocate the digest workspace (faster on large shards;
+    without it the library funnels its partial sums into the result slots).
     """
 
     def __init__(self, param: torch.Tensor, grad: Optional[torch.Tensor], exp_avg: torch.Tensor,
                  exp_avg_sq: torch.Tensor, param_bf16: Optional[torch.Tensor], global_offset: int = 0,
                  segments: Optional[Sequence[Tuple[int, int, int]]] = None,
-                 hypers: Optional[Sequence[Hyper]] = None):
+                 hypers: Optional[Sequence[Hyper]] = None, use_workspace: bool = True):
         n = param.numel()
         f32 = (torch.float32,)
         self.param = _dev_tensor(param, f32, "param", n)
@@ -159,6 +164,11 @@ class Shard:
         else:
             self._csegs = None
             self._chypers = None
+        # digest workspace: lets the partial sums spread over several addresses
+        self.workspace = None
+        if use_workspace:
+            nbytes = int(_lib().pact_workspace_bytes(ctypes.byref(self._c())))
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
 
     def _c(self, digest_out: Optional[torch.Tensor] = None) -> _CShard:
         def ptr(t):
@@ -174,6 +184,9 @@ class Shard:
             s.hypers = ctypes.cast(self._chypers, ctypes.POINTER(_CHyper))
             s.num_hypers = len(self.hypers)
         s.digest_dev = (digest_out if digest_out is not None else self.digest).data_ptr()
+        ws = getattr(self, "workspace", None)
+        if ws is not None:
+            s.workspace, s.workspace_bytes = ws.data_ptr(), ws.numel()
         s.stream = torch.cuda.current_stream(self.device).cuda_stream
         return s
 

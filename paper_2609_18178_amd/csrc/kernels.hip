@@ -1,19 +1,21 @@
 // kernels.hip -- gfx950 kernels of libpactshard.
 //
-// One persistent, grid-stride kernel serves the three modes (commit, state
-// digest, bf16 digest).  Work is cut into tiles of kTile elements that never
-// straddle a segment; workgroup w takes tiles w, w + grid, w + 2*grid, ... so
-// at any moment the whole chip streams one contiguous window of each array.
-// A full, aligned tile moves two 16-byte vectors per array per thread
-// (global_load_dwordx4 / global_store_dwordx4, bf16 as dwordx2); a ragged
-// tail or a misaligned segment goes element by element.
+// One tile kernel serves the three modes (commit, state digest, bf16 digest).
+// Work is cut into tiles of kTile elements that never straddle a segment, and
+// each workgroup takes exactly one tile (the hardware dispatcher then keeps
+// every CU full and balances the tail by itself; a persistent grid measured
+// slower on this pattern).  A full, aligned tile moves two 16-byte vectors
+// per array per thread with buffer_load/store_dwordx4 (bf16: dwordx2) marked
+// non-temporal; a ragged tail or a misaligned segment goes element by element.
 //
 // The digest is accumulated per thread in a 64-bit register (wrapping add),
 // reduced across the wave with shuffles and across the workgroup's four
-// waves through LDS, and added to the caller's slot with one 64-bit atomic
-// per workgroup (per segment when per-segment digests are asked for).
-// Wrapping addition is associative and commutative, so the order in which
-// workgroups arrive cannot change the result.
+// waves through LDS, and added with one 64-bit atomic per workgroup into one
+// of kLanes workspace words of its result slot (256 bytes apart, so the
+// atomics of neighbouring workgroups do not queue on one address); a final
+// one-workgroup kernel sums the lanes.  Without a workspace the atomics go to
+// the result slot itself.  Wrapping addition is associative and commutative,
+// so the order in which workgroups arrive cannot change the result.
 //
 // Arithmetic is the library contract in pactshard.h: one IEEE binary32
 // rounding per operation, no contraction or reassociation (the translation
@@ -98,12 +100,46 @@ __device__ __forceinline__ uint64_t block_sum(uint64_t x, uint64_t* lds) {
             r += lds[w];
         }
     }
-    __syncthreads();
     return r;
 }
 
 // ---------------------------------------------------------------------------
-// one element, element-wise path
+// HBM access: raw buffer instructions on a per-tile resource (base address in
+// scalar registers, 32-bit byte offset per lane), with the non-temporal cache
+// policy on loads and stores -- every byte is touched exactly once.
+// ---------------------------------------------------------------------------
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kRsrcWord3 = 0x00020000;  // raw, untyped buffer (gfx9 family)
+constexpr int kNonTemporal = 2;         // cache-policy 'nt' bit
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+// The whole byte offset travels in the per-lane VGPR offset and the scalar
+// offset field stays the literal 0.  That matters for stores wider than 8
+// bytes: their data VGPRs must not be overwritten by the very next VALU
+// instruction (one wait state), and the compiler only guards that hazard
+// when the scalar offset is not a register.  With a register scalar offset a
+// following VALU write was seen to corrupt the first dword of the stored
+// vector.
+__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kNonTemporal);
+}
+__device__ __forceinline__ void store16(u32x4 x, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b128(x, r, (int)off, 0, kNonTemporal);
+}
+__device__ __forceinline__ u32x2 load8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kNonTemporal);
+}
+__device__ __forceinline__ void store8(u32x2 x, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)off, 0, kNonTemporal);
+}
+
+// ---------------------------------------------------------------------------
+// one element, element-wise path (ragged tails, misaligned segments)
 // ---------------------------------------------------------------------------
 template <Mode M>
 __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const StepScalars& sc) {
@@ -127,173 +163,241 @@ __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const
 }
 
 // ---------------------------------------------------------------------------
-// one full aligned tile, vector path: kUnroll x 16-byte vectors per array
+// one full tile whose start is 16-byte aligned in every fp32 array (8-byte in
+// the bf16 array): kUnroll rows of kBlock 16-byte vectors per array.  Row u,
+// lane t holds elements e0 + u*kBlock*4 + 4t .. +3.
 // ---------------------------------------------------------------------------
 template <Mode M>
 __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, const StepScalars& sc) {
+    constexpr uint32_t kRow32 = kBlock * kVec * 4;  // bytes of one fp32 row
+    constexpr uint32_t kRow16 = kBlock * kVec * 2;  // bytes of one bf16 row
+    const uint32_t lane32 = threadIdx.x * kVec * 4;
+    const uint32_t lane16 = threadIdx.x * kVec * 2;
+    const uint64_t lane_idx = a.goff + e0 + threadIdx.x * kVec;
     uint64_t acc = 0;
     if constexpr (M == Mode::Bf16Digest) {
+        const auto rb = tile_rsrc(a.b + e0, kTile * 2);
+        u32x2 W[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint64_t e = e0 + (uint64_t)(u * kBlock * kVec) + threadIdx.x * kVec;
-            const uint2 w = *reinterpret_cast<const uint2*>(a.b + e);
-            const uint64_t idx = a.goff + e;
-            acc += hash_word(w.x & 0xFFFFu, idx | kTagB) + hash_word(w.x >> 16, (idx + 1) | kTagB) +
-                   hash_word(w.y & 0xFFFFu, (idx + 2) | kTagB) + hash_word(w.y >> 16, (idx + 3) | kTagB);
+            W[u] = load8(rb, lane16 + u * kRow16);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint64_t i = lane_idx + (uint64_t)u * kBlock * kVec;
+            acc += hash_word(W[u].x & 0xFFFFu, i | kTagB) + hash_word(W[u].x >> 16, (i + 1) | kTagB) +
+                   hash_word(W[u].y & 0xFFFFu, (i + 2) | kTagB) + hash_word(W[u].y >> 16, (i + 3) | kTagB);
         }
         return acc;
     } else {
-        float4 P[kUnroll], G[kUnroll], Mo[kUnroll], V[kUnroll];
+        const auto rp = tile_rsrc(a.p + e0, kTile * 4);
+        const auto rm = tile_rsrc(a.m + e0, kTile * 4);
+        const auto rv = tile_rsrc(a.v + e0, kTile * 4);
+        u32x4 P[kUnroll], G[kUnroll], Mo[kUnroll], V[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint64_t e = e0 + (uint64_t)(u * kBlock * kVec) + threadIdx.x * kVec;
-            P[u] = *reinterpret_cast<const float4*>(a.p + e);
-            Mo[u] = *reinterpret_cast<const float4*>(a.m + e);
-            V[u] = *reinterpret_cast<const float4*>(a.v + e);
-            if constexpr (M == Mode::Commit) {
-                G[u] = *reinterpret_cast<const float4*>(a.g + e);
+            P[u] = load16(rp, lane32 + u * kRow32);
+            Mo[u] = load16(rm, lane32 + u * kRow32);
+            V[u] = load16(rv, lane32 + u * kRow32);
+        }
+        if constexpr (M == Mode::Commit) {
+            const auto rg = tile_rsrc(a.g + e0, kTile * 4);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                G[u] = load16(rg, lane32 + u * kRow32);
+            }
+            const auto rb = tile_rsrc(a.b + e0, kTile * 2);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                float p[4], m[4], v[4];
+#pragma unroll
+                for (int j = 0; j < kVec; ++j) {
+                    p[j] = __uint_as_float(P[u][j]);
+                    m[j] = __uint_as_float(Mo[u][j]);
+                    v[j] = __uint_as_float(V[u][j]);
+                    adamw(p[j], __uint_as_float(G[u][j]), m[j], v[j], sc);
+                    P[u][j] = __float_as_uint(p[j]);
+                    Mo[u][j] = __float_as_uint(m[j]);
+                    V[u][j] = __float_as_uint(v[j]);
+                }
+                store16(P[u], rp, lane32 + u * kRow32);
+                store16(Mo[u], rm, lane32 + u * kRow32);
+                store16(V[u], rv, lane32 + u * kRow32);
+                u32x2 h;
+                h.x = to_bf16(p[0]) | (to_bf16(p[1]) << 16);
+                h.y = to_bf16(p[2]) | (to_bf16(p[3]) << 16);
+                store8(h, rb, lane16 + u * kRow16);
             }
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint64_t e = e0 + (uint64_t)(u * kBlock * kVec) + threadIdx.x * kVec;
-            if constexpr (M == Mode::Commit) {
-                adamw(P[u].x, G[u].x, Mo[u].x, V[u].x, sc);
-                adamw(P[u].y, G[u].y, Mo[u].y, V[u].y, sc);
-                adamw(P[u].z, G[u].z, Mo[u].z, V[u].z, sc);
-                adamw(P[u].w, G[u].w, Mo[u].w, V[u].w, sc);
-                *reinterpret_cast<float4*>(a.p + e) = P[u];
-                *reinterpret_cast<float4*>(a.m + e) = Mo[u];
-                *reinterpret_cast<float4*>(a.v + e) = V[u];
-                uint2 h;
-                h.x = to_bf16(P[u].x) | (to_bf16(P[u].y) << 16);
-                h.y = to_bf16(P[u].z) | (to_bf16(P[u].w) << 16);
-                *reinterpret_cast<uint2*>(a.b + e) = h;
-            }
-            const uint64_t idx = a.goff + e;
-            const float pv[4] = {P[u].x, P[u].y, P[u].z, P[u].w};
-            const float mv[4] = {Mo[u].x, Mo[u].y, Mo[u].z, Mo[u].w};
-            const float vv[4] = {V[u].x, V[u].y, V[u].z, V[u].w};
 #pragma unroll
             for (int j = 0; j < kVec; ++j) {
-                const uint64_t i = idx + j;
-                acc += hash_word(__float_as_uint(pv[j]), i) + hash_word(__float_as_uint(mv[j]), i | kTagM) +
-                       hash_word(__float_as_uint(vv[j]), i | kTagV);
+                const uint64_t i = lane_idx + (uint64_t)u * kBlock * kVec + j;
+                acc += hash_word(P[u][j], i) + hash_word(Mo[u][j], i | kTagM) + hash_word(V[u][j], i | kTagV);
             }
         }
         return acc;
     }
 }
 
+// ---------------------------------------------------------------------------
+// One workgroup per tile.  The tile's segment is found by binary search over
+// the batch's tile prefix (kernel arguments, scalar loads); the tile's digest
+// share is reduced across the workgroup and added to the segment's slot (or
+// the single total slot) with one 64-bit atomic.
+// ---------------------------------------------------------------------------
 template <Mode M>
-__global__ __launch_bounds__(kBlock) void shard_kernel(Arrays a, Batch bt) {
+__global__ __launch_bounds__(kBlock) void tile_kernel(Arrays a, Batch bt) {
     __shared__ uint64_t lds[kBlock / 64];
-    const uint64_t ntiles = bt.tile_begin[bt.nseg];
-    uint32_t seg = 0;
-    uint64_t seg_acc = 0;  // this thread's share of the current segment
-    uint64_t all_acc = 0;  // this thread's share of the launch's segments
-
-    for (uint64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        // tile and seg are uniform across the workgroup
-        while (tile >= bt.tile_begin[seg + 1]) {
-            if (bt.per_segment) {
-                const uint64_t s = block_sum(seg_acc, lds);
-                if (threadIdx.x == 0 && s != 0) {
-                    atomicAdd(reinterpret_cast<unsigned long long*>(a.digest + bt.slot0 + seg),
-                              (unsigned long long)s);
-                }
-            }
-            all_acc += seg_acc;
-            seg_acc = 0;
-            ++seg;
-        }
-        const StepScalars sc = bt.sc[seg];
-        const uint64_t seg_first = bt.elem_begin[seg];
-        const uint64_t seg_end = seg_first + bt.elem_count[seg];
-        const uint64_t e0 = seg_first + (tile - bt.tile_begin[seg]) * (uint64_t)kTile;
-        if (bt.vec_ok[seg] && e0 + kTile <= seg_end) {
-            seg_acc += do_tile_vec<M>(a, e0, sc);
+    const uint64_t tile = blockIdx.x;
+    uint32_t lo = 0, hi = bt.nseg;  // largest lo with tile_begin[lo] <= tile
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (tile >= bt.tile_begin[mid]) {
+            lo = mid;
         } else {
-            const uint64_t e1 = (e0 + kTile < seg_end) ? e0 + kTile : seg_end;
-            for (uint64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-                seg_acc += do_scalar<M>(a, e, sc);
+            hi = mid;
+        }
+    }
+    const uint32_t seg = lo;
+    const StepScalars sc = bt.sc[seg];
+    const uint64_t seg_first = bt.elem_begin[seg];
+    const uint64_t seg_end = seg_first + bt.elem_count[seg];
+    const uint64_t e0 = seg_first + (tile - bt.tile_begin[seg]) * (uint64_t)kTile;
+    uint64_t acc = 0;
+    if (bt.vec_ok[seg] && e0 + kTile <= seg_end) {
+        acc = do_tile_vec<M>(a, e0, sc);
+    } else {
+        const uint64_t e1 = (e0 + kTile < seg_end) ? e0 + kTile : seg_end;
+        for (uint64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+            acc += do_scalar<M>(a, e, sc);
+        }
+    }
+    const uint64_t s = block_sum(acc, lds);
+    if (threadIdx.x == 0 && s != 0) {
+        const uint64_t r = bt.per_segment ? bt.slot0 + seg : 0;
+        uint64_t* dst = a.lanes ? a.lanes + (r * kLanes + (blockIdx.x & (kLanes - 1))) * kLaneStride : a.digest + r;
+        atomicAdd(reinterpret_cast<unsigned long long*>(dst), (unsigned long long)s);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void clear_kernel(uint64_t* digest, uint64_t* lanes, uint32_t nres,
+                                                       uint32_t nslots) {
+    if (lanes) {
+        const uint32_t n = nres * kLanes;
+        for (uint32_t i = threadIdx.x; i < n; i += kBlock) {
+            lanes[(uint64_t)i * kLaneStride] = 0;
+        }
+    } else {
+        for (uint32_t i = threadIdx.x; i < nslots; i += kBlock) {
+            digest[i] = 0;
+        }
+    }
+}
+
+// digest[r] = sum of r's lanes for r < nres (when lanes are used); with
+// per-segment results also digest[nres] = sum of digest[0..nres).
+__global__ __launch_bounds__(kBlock) void finish_kernel(uint64_t* digest, const uint64_t* lanes, uint32_t nres,
+                                                        uint32_t per_segment) {
+    __shared__ uint64_t lds[kBlock / 64];
+    uint64_t total = 0;
+    for (uint32_t r = threadIdx.x; r < nres; r += kBlock) {
+        uint64_t x;
+        if (lanes) {
+            x = 0;
+            for (int l = 0; l < kLanes; ++l) {
+                x += lanes[((uint64_t)r * kLanes + l) * kLaneStride];
             }
+            digest[r] = x;
+        } else {
+            x = digest[r];
         }
+        total += x;
     }
-    // flush the last segment this workgroup touched and the launch total
-    if (bt.per_segment) {
-        const uint64_t s = block_sum(seg_acc, lds);
-        if (threadIdx.x == 0 && s != 0) {
-            atomicAdd(reinterpret_cast<unsigned long long*>(a.digest + bt.slot0 + seg), (unsigned long long)s);
+    if (per_segment) {
+        const uint64_t t = block_sum(total, lds);
+        if (threadIdx.x == 0) {
+            digest[nres] = t;
         }
-    }
-    all_acc += seg_acc;
-    const uint64_t t = block_sum(all_acc, lds);
-    if (threadIdx.x == 0 && t != 0) {
-        atomicAdd(reinterpret_cast<unsigned long long*>(a.digest + bt.total_slot), (unsigned long long)t);
     }
 }
 
-__global__ void zero_kernel(uint64_t* slots, uint32_t n) {
-    for (uint32_t i = threadIdx.x; i < n; i += blockDim.x) {
-        slots[i] = 0;
-    }
-}
-
-// 30 bytes per element, no arithmetic beyond one add: the ceiling of the
-// commit's access pattern.
-// The outputs may alias the inputs element for element (in place).
+// 30 bytes per element with no arithmetic beyond one add, through the same
+// instructions, tile shape and launch shape as the commit: the ceiling of the
+// commit's access pattern.  The outputs may alias the inputs element for
+// element (in place).  n is a multiple of 4; the last tile's resources end at
+// n, and a vector beyond it is dropped by the buffer range check.
 __global__ __launch_bounds__(kBlock) void probe_kernel(const float* i0, const float* i1, const float* i2,
                                                        const float* i3, float* o0, float* o2, float* o3,
-                                                       uint16_t* oh, uint64_t nvec) {
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-    for (uint64_t k = (uint64_t)blockIdx.x * kBlock + threadIdx.x; k < nvec; k += stride) {
-        const float4 a = reinterpret_cast<const float4*>(i0)[k];
-        const float4 b = reinterpret_cast<const float4*>(i1)[k];
-        const float4 c = reinterpret_cast<const float4*>(i2)[k];
-        const float4 d = reinterpret_cast<const float4*>(i3)[k];
-        float4 s;
-        s.x = a.x + b.x;
-        s.y = a.y + b.y;
-        s.z = a.z + b.z;
-        s.w = a.w + b.w;
-        reinterpret_cast<float4*>(o0)[k] = s;
-        reinterpret_cast<float4*>(o2)[k] = c;
-        reinterpret_cast<float4*>(o3)[k] = d;
-        uint2 h;
-        h.x = (__float_as_uint(s.x) >> 16) | (__float_as_uint(s.y) & 0xFFFF0000u);
-        h.y = (__float_as_uint(s.z) >> 16) | (__float_as_uint(s.w) & 0xFFFF0000u);
-        reinterpret_cast<uint2*>(oh)[k] = h;
+                                                       uint16_t* oh, uint64_t n) {
+    constexpr uint32_t kRow32 = kBlock * kVec * 4;
+    constexpr uint32_t kRow16 = kBlock * kVec * 2;
+    const uint64_t e0 = (uint64_t)blockIdx.x * kTile;
+    const uint64_t left = n - e0;
+    const uint32_t cnt = left < (uint64_t)kTile ? (uint32_t)left : (uint32_t)kTile;
+    const auto r0 = tile_rsrc(i0 + e0, cnt * 4), r1 = tile_rsrc(i1 + e0, cnt * 4);
+    const auto r2 = tile_rsrc(i2 + e0, cnt * 4), r3 = tile_rsrc(i3 + e0, cnt * 4);
+    const auto w0 = tile_rsrc(o0 + e0, cnt * 4), w2 = tile_rsrc(o2 + e0, cnt * 4);
+    const auto w3 = tile_rsrc(o3 + e0, cnt * 4), wh = tile_rsrc(oh + e0, cnt * 2);
+    const uint32_t lane32 = threadIdx.x * kVec * 4, lane16 = threadIdx.x * kVec * 2;
+    u32x4 A[kUnroll], B[kUnroll], C[kUnroll], D[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        A[u] = load16(r0, lane32 + u * kRow32);
+        B[u] = load16(r1, lane32 + u * kRow32);
+        C[u] = load16(r2, lane32 + u * kRow32);
+        D[u] = load16(r3, lane32 + u * kRow32);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        u32x4 s;
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+            s[j] = __float_as_uint(__uint_as_float(A[u][j]) + __uint_as_float(B[u][j]));
+        }
+        store16(s, w0, lane32 + u * kRow32);
+        store16(C[u], w2, lane32 + u * kRow32);
+        store16(D[u], w3, lane32 + u * kRow32);
+        u32x2 h;
+        h.x = (s.x >> 16) | (s.y & 0xFFFF0000u);
+        h.y = (s.z >> 16) | (s.w & 0xFFFF0000u);
+        store8(h, wh, lane16 + u * kRow16);
     }
 }
 
 }  // namespace
 
-hipError_t launch_zero(uint64_t* slots, uint32_t nslots, hipStream_t stream) {
-    hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(256), 0, stream, slots, nslots);
+hipError_t launch_clear(uint64_t* digest, uint64_t* lanes, uint32_t nres, uint32_t nslots, hipStream_t stream) {
+    hipLaunchKernelGGL(clear_kernel, dim3(1), dim3(kBlock), 0, stream, digest, lanes, nres, nslots);
     return hipGetLastError();
 }
 
 hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t grid, hipStream_t stream) {
     switch (mode) {
         case Mode::Commit:
-            hipLaunchKernelGGL(shard_kernel<Mode::Commit>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            hipLaunchKernelGGL(tile_kernel<Mode::Commit>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
         case Mode::StateDigest:
-            hipLaunchKernelGGL(shard_kernel<Mode::StateDigest>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            hipLaunchKernelGGL(tile_kernel<Mode::StateDigest>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
         case Mode::Bf16Digest:
-            hipLaunchKernelGGL(shard_kernel<Mode::Bf16Digest>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            hipLaunchKernelGGL(tile_kernel<Mode::Bf16Digest>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
     }
     return hipGetLastError();
 }
 
+hipError_t launch_finish(uint64_t* digest, uint64_t* lanes, uint32_t nres, bool per_segment, hipStream_t stream) {
+    hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(kBlock), 0, stream, digest, lanes, nres, per_segment ? 1u : 0u);
+    return hipGetLastError();
+}
+
 hipError_t launch_probe(const float* i0, const float* i1, const float* i2, const float* i3,
-                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n,
-                        uint32_t grid, hipStream_t stream) {
-    hipLaunchKernelGGL(probe_kernel, dim3(grid), dim3(kBlock), 0, stream, i0, i1, i2, i3, o0, o2, o3, oh,
-                       n / kVec);
+                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, hipStream_t stream) {
+    const uint64_t tiles = (n + kTile - 1) / kTile;
+    hipLaunchKernelGGL(probe_kernel, dim3((uint32_t)tiles), dim3(kBlock), 0, stream, i0, i1, i2, i3, o0, o2, o3,
+                       oh, n);
     return hipGetLastError();
 }
 

@@ -13,11 +13,16 @@ namespace pact {
 constexpr int kSegsPerLaunch = 32;
 
 // Threads per workgroup (4 waves of 64) and fp32 elements one thread moves
-// per tile: two 16-byte vectors per array.
+// per tile: four 16-byte vectors per array.
 constexpr int kBlock = 256;
 constexpr int kVec = 4;
-constexpr int kUnroll = 2;
-constexpr int kTile = kBlock * kVec * kUnroll;  // 2048 elements per tile
+constexpr int kUnroll = 4;
+constexpr int kTile = kBlock * kVec * kUnroll;  // 4096 elements per tile
+
+// Digest partial sums: each result slot owns kLanes workspace words,
+// kLaneStride words (256 bytes) apart; workgroup w adds into lane w % kLanes.
+constexpr int kLanes = 16;
+constexpr int kLaneStride = 32;
 
 // Per-segment binary32 scalars of one step.
 struct StepScalars {
@@ -28,9 +33,8 @@ struct StepScalars {
 // segment s owns tiles [tile_begin[s], tile_begin[s+1]).
 struct Batch {
     uint32_t nseg;
-    uint32_t slot0;        // digest slot of this batch's first segment
-    uint32_t total_slot;   // slot of the sum over all segments
-    uint32_t per_segment;  // nonzero: also write per-segment slots
+    uint32_t slot0;        // result slot of this batch's first segment
+    uint32_t per_segment;  // nonzero: one result slot per segment, else one in all
     uint64_t tile_begin[kSegsPerLaunch + 1];
     uint64_t elem_begin[kSegsPerLaunch];  // shard-relative first element
     uint64_t elem_count[kSegsPerLaunch];
@@ -45,20 +49,26 @@ struct Arrays {
     float* v;
     uint16_t* b;
     uint64_t goff;      // global flat index of shard element 0
-    uint64_t* digest;   // slots
+    uint64_t* digest;   // result slots
+    uint64_t* lanes;    // workspace lanes, or null: atomics go to the result slots
 };
 
 enum class Mode : int { Commit = 0, StateDigest = 1, Bf16Digest = 2 };
 
-// Enqueue: zero `nslots` digest slots.
-hipError_t launch_zero(uint64_t* slots, uint32_t nslots, hipStream_t stream);
+// Enqueue the clearing of what the tile kernels accumulate into: the
+// nres * kLanes lane words when `lanes` is given, else the nslots digest slots.
+hipError_t launch_clear(uint64_t* digest, uint64_t* lanes, uint32_t nres, uint32_t nslots, hipStream_t stream);
 
-// Enqueue one batch in the given mode on `grid` workgroups.
+// Enqueue one batch in the given mode: one workgroup per tile, so `grid` is
+// the batch's tile count.
 hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t grid, hipStream_t stream);
 
-// Enqueue the 30-byte/element stream probe.
+// Enqueue the final sums: digest[r] = sum of r's lanes (when `lanes` is
+// given) for r < nres, and, with per-segment results, digest[nres] = their sum.
+hipError_t launch_finish(uint64_t* digest, uint64_t* lanes, uint32_t nres, bool per_segment, hipStream_t stream);
+
+// Enqueue the 30-byte/element stream probe (n a multiple of kVec).
 hipError_t launch_probe(const float* i0, const float* i1, const float* i2, const float* i3,
-                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n,
-                        uint32_t grid, hipStream_t stream);
+                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, hipStream_t stream);
 
 }  // namespace pact

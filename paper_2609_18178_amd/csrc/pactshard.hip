@@ -6,7 +6,6 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
-#include <mutex>
 #include <vector>
 
 #include "launch.h"
@@ -16,31 +15,11 @@ namespace {
 thread_local int g_last_hip_error = 0;
 
 constexpr uint64_t kIndexLimit = 1ull << 56;  // indices must stay below the tag bits
+constexpr uint32_t kMaxSegments = 1u << 24;     // keeps every slot and lane index in 32 bits
 
 int fail_hip(hipError_t e) {
     g_last_hip_error = static_cast<int>(e);
     return PACT_EHIP;
-}
-
-// ---------------------------------------------------------------------------
-// launch geometry: persistent workgroups per compute unit, per device
-// ---------------------------------------------------------------------------
-constexpr int kMaxDevices = 64;
-constexpr uint32_t kGroupsPerCu = 8;
-
-int g_cus[kMaxDevices];
-std::once_flag g_cu_once[kMaxDevices];
-
-int cu_count(int dev) {
-    if (dev < 0 || dev >= kMaxDevices) return 256;
-    std::call_once(g_cu_once[dev], [dev] {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
-            n = 256;
-        }
-        g_cus[dev] = n;
-    });
-    return g_cus[dev];
 }
 
 // ---------------------------------------------------------------------------
@@ -69,6 +48,14 @@ bool overlaps(const std::vector<Span>& spans) {
     return false;
 }
 
+// Result slots that accumulate partial sums (one per segment, or one), and
+// the workspace bytes their lanes take.
+uint64_t result_slots(const pact_shard* s) { return s->segs ? (uint64_t)s->num_segs : 1; }
+
+uint64_t workspace_need(const pact_shard* s) {
+    return result_slots(s) * pact::kLanes * pact::kLaneStride * sizeof(uint64_t);
+}
+
 // Which arrays a mode touches.
 struct Uses {
     bool p, g, m, v, b;
@@ -87,8 +74,11 @@ int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t
     }
     if (s->global_offset >= kIndexLimit || n > kIndexLimit - s->global_offset) return PACT_ERANGE;
     if (n > (UINT64_MAX / 4)) return PACT_ERANGE;
+    if ((n + pact::kTile - 1) / pact::kTile + (s->segs ? s->num_segs : 1) > (uint64_t)INT32_MAX) {
+        return PACT_ERANGE;  // more tiles than one launch grid can hold
+    }
     if (s->segs != nullptr) {
-        if (s->num_segs == 0 || s->num_segs > 0x7FFFFFFFu) return PACT_EINVAL;
+        if (s->num_segs == 0 || s->num_segs > kMaxSegments) return PACT_EINVAL;
         uint64_t prev_end = 0;
         for (uint32_t k = 0; k < s->num_segs; ++k) {
             const pact_segment& sg = s->segs[k];
@@ -104,6 +94,10 @@ int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t
         return PACT_EALIGN;
     }
     const uint64_t slots = s->segs ? (uint64_t)s->num_segs + 1 : 1;
+    if (s->workspace != nullptr) {
+        if (!aligned(s->workspace, 8)) return PACT_EALIGN;
+        if (s->workspace_bytes < workspace_need(s)) return PACT_EINVAL;
+    }
     std::vector<Span> spans;
     auto add = [&](const void* ptr, uint64_t bytes) {
         if (ptr && bytes) {
@@ -117,6 +111,7 @@ int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t
     if (use.v) add(s->exp_avg_sq, n * 4);
     if (use.b) add(s->param_bf16, n * 2);
     add(out, slots * 8);
+    if (s->workspace != nullptr) add(s->workspace, workspace_need(s));
     for (const Span& sp : spans) {
         if (sp.hi < sp.lo) return PACT_ERANGE;  // wraps the address space
     }
@@ -164,12 +159,9 @@ struct SegWork {
 
 int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots) {
     hipStream_t stream = static_cast<hipStream_t>(s->stream);
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fail_hip(e);
-    const uint32_t max_grid = (uint32_t)cu_count(dev) * kGroupsPerCu;
-
-    e = pact::launch_zero(out, (uint32_t)nslots, stream);
+    uint64_t* lanes = static_cast<uint64_t*>(s->workspace);
+    const uint32_t nres = (uint32_t)result_slots(s);
+    hipError_t e = pact::launch_clear(out, lanes, nres, (uint32_t)nslots, stream);
     if (e != hipSuccess) return fail_hip(e);
 
     pact::Arrays a;
@@ -180,16 +172,15 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
     a.b = s->param_bf16;
     a.goff = s->global_offset;
     a.digest = out;
+    a.lanes = lanes;
 
     const bool per_segment = s->segs != nullptr;
-    const uint32_t total_slot = (uint32_t)(nslots - 1);
     for (size_t first = 0; first < work.size(); first += pact::kSegsPerLaunch) {
         const size_t cnt = std::min<size_t>(pact::kSegsPerLaunch, work.size() - first);
         pact::Batch b;
         std::memset(&b, 0, sizeof b);
         b.nseg = (uint32_t)cnt;
         b.slot0 = (uint32_t)first;
-        b.total_slot = total_slot;
         b.per_segment = per_segment ? 1u : 0u;
         uint64_t tiles = 0;
         for (size_t k = 0; k < cnt; ++k) {
@@ -212,8 +203,11 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
         }
         b.tile_begin[cnt] = tiles;
         if (tiles == 0) continue;
-        const uint32_t grid = (uint32_t)std::min<uint64_t>(tiles, max_grid);
-        e = pact::launch_batch(mode, a, b, grid, stream);
+        e = pact::launch_batch(mode, a, b, (uint32_t)tiles, stream);
+        if (e != hipSuccess) return fail_hip(e);
+    }
+    if (lanes != nullptr || per_segment) {
+        e = pact::launch_finish(out, lanes, nres, per_segment, stream);
         if (e != hipSuccess) return fail_hip(e);
     }
     return PACT_OK;
@@ -258,6 +252,11 @@ int64_t pact_digest_slots(const pact_shard* s) {
     return s->segs ? (int64_t)s->num_segs + 1 : 1;
 }
 
+int64_t pact_workspace_bytes(const pact_shard* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    return (int64_t)workspace_need(s);
+}
+
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
     if (s == nullptr || step == 0) return PACT_EINVAL;
     if (s->segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
@@ -299,14 +298,9 @@ int pact_stream_probe(const float* in0, const float* in1, const float* in2, cons
         !aligned(out2, 16) || !aligned(out3, 16) || !aligned(out_half, 8)) {
         return PACT_EALIGN;
     }
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fail_hip(e);
-    const uint64_t nvec = n / pact::kVec;
-    const uint64_t groups = (nvec + pact::kBlock - 1) / pact::kBlock;
-    const uint32_t grid = (uint32_t)std::min<uint64_t>(groups, (uint64_t)cu_count(dev) * kGroupsPerCu);
-    e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n, grid,
-                           static_cast<hipStream_t>(stream));
+    if ((n + pact::kTile - 1) / pact::kTile > (uint64_t)INT32_MAX) return PACT_ERANGE;
+    hipError_t e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n,
+                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail_hip(e);
     return PACT_OK;
 }

@@ -141,6 +141,28 @@ def test_digest_slots():
     assert commit(s, h=None) == pk.PACT_EOVERLAP
 
 
+def test_workspace_contract():
+    lib = pk._lib()
+    s = fake_shard()
+    need = lib.pact_workspace_bytes(ctypes.byref(s))
+    assert need == 16 * 32 * 8
+    seg = _with_segs([(0, 10, 0, 0), (16, 4, 0, 0), (100, 0, 0, 0)])
+    assert lib.pact_workspace_bytes(ctypes.byref(seg)) == 3 * need
+    ws = BASE + 6 * SPAN
+    assert commit(fake_shard(workspace=ws, workspace_bytes=need - 8)) == pk.PACT_EINVAL
+    assert commit(fake_shard(workspace=ws + 4, workspace_bytes=need)) == pk.PACT_EALIGN
+    assert commit(fake_shard(workspace=BASE + 2 * SPAN + 1024, workspace_bytes=need)) == pk.PACT_EOVERLAP
+    assert commit(fake_shard(workspace=BASE + 5 * SPAN, workspace_bytes=need)) == pk.PACT_EOVERLAP
+    assert lib.pact_workspace_bytes(None) == pk.PACT_EINVAL
+
+
+def test_segment_count_limit():
+    s = fake_shard()
+    s.segs = ctypes.cast((_CSegment * 1)(), ctypes.POINTER(_CSegment))
+    s.num_segs = (1 << 24) + 1
+    assert commit(s, h=None) == pk.PACT_EINVAL
+
+
 def test_probe_errors():
     lib = pk._lib()
     a = [BASE + k * SPAN for k in range(8)]

@@ -93,6 +93,32 @@ def test_ragged_and_unaligned(n, shift):
         assert not h[:shift].any() and not h[shift + n:].any()
 
 
+@pytest.mark.parametrize("segmented", [False, True])
+def test_without_workspace(segmented):
+    """workspace == NULL: partial sums go straight to the result slots; the
+    results are the same bits."""
+    import torch
+
+    pk = _pk()
+    w = wl.shrunken_mistral() if segmented else wl.WORKLOADS["tiny"]
+    p, g, m, v = wl.arrays_host(w)
+    segs = w.segments if segmented else None
+    hyp = [pk.Hyper(**h) for h in w.hypers] if segmented else None
+    t = [torch.from_numpy(a).cuda() for a in (p, g, m, v)]
+    sh = pk.Shard(*t, torch.zeros(p.size, dtype=torch.int16, device="cuda"), w.global_offset,
+                  segments=segs, hypers=hyp, use_workspace=False)
+    assert sh.workspace is None
+    got = pk.to_u64(pk.adamw_commit(sh, w.first_step, None if segmented else g_hyper(H)))
+    b = np.zeros(p.size, np.uint16)
+    if segmented:
+        per, total = oracle.commit_segments(p, g, m, v, b, w.segments, [o_hyper(h) for h in w.hypers],
+                                            w.first_step, w.global_offset)
+        assert got == per + [total]
+    else:
+        assert got == [oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), w.first_step, w.global_offset)]
+    _compare_full(sh, p, m, v, b)
+
+
 def test_empty_shard():
     """n = 0: the digest is 0 and nothing is read or written."""
     import torch
