@@ -47,7 +47,62 @@ def parse():
                     help="target seconds for each CPU oracle leg (single thread, all threads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) of a "
+                         "bench run into profiles/traffic_<workload>.json and exit")
     return ap.parse_args()
+
+
+COMMIT_KERNEL = "tile_kernel<(pact::Mode)0>"
+PROBE_KERNEL = "probe_kernel("
+
+
+def _counter_values(path: str, counter: str):
+    import csv
+
+    out = {}
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] != counter:
+                continue
+            name = row["Kernel_Name"]
+            key = "commit" if COMMIT_KERNEL in name else "probe" if PROBE_KERNEL in name else None
+            if key:
+                out.setdefault(key, []).append(float(row["Counter_Value"]) * 1024.0)  # KiB -> bytes
+    return out
+
+
+def record_traffic(workload: str, fetch_csv: str, write_csv: str) -> dict:
+    """HBM bytes per commit launch from FETCH_SIZE and WRITE_SIZE, each scaled
+    by what the same counter reads for the stream probe, whose bytes are known
+    exactly (16 fetched and 14 written per element)."""
+    import workloads as wl
+
+    n = wl.WORKLOADS[workload].numel
+    f = _counter_values(fetch_csv, "FETCH_SIZE")
+    w = _counter_values(write_csv, "WRITE_SIZE")
+    mean = lambda xs: sum(xs) / len(xs)  # noqa: E731
+    f_scale = 16.0 * n / mean(f["probe"])
+    w_scale = 14.0 * n / mean(w["probe"])
+    fetch = mean(f["commit"]) * f_scale
+    write = mean(w["commit"]) * w_scale
+    rec = {
+        "workload": workload,
+        "kernel_source_hash": kernel_source_hash(),
+        "bytes_per_launch": fetch + write,
+        "fetch_bytes_per_launch": fetch,
+        "write_bytes_per_launch": write,
+        "algorithmic_bytes_per_launch": BYTES_PER_ELEM * n,
+        "fetch_scale": f_scale,
+        "write_scale": w_scale,
+        "commit_dispatches": [len(f["commit"]), len(w["commit"])],
+        "probe_dispatches": [len(f["probe"]), len(w["probe"])],
+    }
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    return rec
 
 
 def cpu_baseline(w, seconds: float) -> dict:
@@ -128,6 +183,9 @@ def stored_traffic(workload: str, src_hash: str):
 
 def main():
     args = parse()
+    if args.record_traffic:
+        print(json.dumps(record_traffic(args.workload, *args.record_traffic)))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the commit of a "
               "rank's shard needs no communication, and sharding across GPUs is not part of this build.",
