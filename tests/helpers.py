@@ -91,3 +91,47 @@ def assert_bitwise(name, got: np.ndarray, want: np.ndarray) -> None:
         i = int(bad[0])
         raise AssertionError(f"{name}: {bad.size} of {gb.size} elements differ; first at {i}: "
                              f"got {int(gb[i]):#x} want {int(wb[i]):#x}")
+
+
+def oracle_stream_segments(w, step: int, hypers, chunk: int = 1 << 26, check=None):
+    """The oracle over a workload's segments, chunk by chunk: each chunk's
+    inputs are drawn on the host (same generator, same global indices as the
+    device arrays), committed by the oracle cut over host threads, and its
+    state and bf16 digests added to its segment.  Memory stays at one chunk.
+    ``check(start, p, m, v, b)``, if given, sees each committed chunk."""
+    segs = w.segments if w.segments is not None else ((0, w.numel, 0),)
+    per, per_b = [], []
+    threads = host_threads()
+    for off, length, hi in segs:
+        d = db = 0
+        for a in range(off, off + length, chunk):
+            cnt = min(chunk, off + length - a)
+            p, g, m, v = wl.arrays_host(w, a, cnt)
+            if step != w.first_step:
+                g = wl.grad_host(w, step, a, cnt)
+            b = np.zeros(cnt, np.uint16)
+            d += oracle_commit_parallel(p, g, m, v, b, hypers[hi], step, w.global_offset + a,
+                                        parts=threads if cnt >= (1 << 20) else 1)
+            db += oracle.bf16_digest(b, w.global_offset + a)
+            if check is not None:
+                check(a, p, m, v, b)
+        per.append(d & M64)
+        per_b.append(db & M64)
+    return per, per_b
+
+
+def device_workload(w, device="cuda"):
+    """Device arrays of a workload filled chunk by chunk from the host
+    generator, and the Shard over them."""
+    import torch
+    import paper_2609_18178_amd as pk
+
+    n = w.numel
+    ts = [torch.empty(n, dtype=torch.float32, device=device) for _ in range(4)]
+    for t, aid, step, dist in zip(ts, (wl.ARRAY_PARAM, wl.ARRAY_GRAD, wl.ARRAY_EXP_AVG, wl.ARRAY_EXP_AVG_SQ),
+                                  (0, w.first_step, 0, 0), (w.param, w.grad, w.exp_avg, w.exp_avg_sq)):
+        wl.fill_device(t, w.global_offset, w.seed, aid, step, dist)
+    b = torch.zeros(n, dtype=torch.int16, device=device)
+    segs = list(w.segments) if w.segments is not None else None
+    hyp = [g_hyper(h) for h in w.hypers] if segs is not None else None
+    return pk.Shard(*ts, b, global_offset=w.global_offset, segments=segs, hypers=hyp)

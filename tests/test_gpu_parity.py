@@ -354,29 +354,3 @@ def test_stream_probe_moves_the_bytes():
     assert torch.equal(a, ref[0]) and torch.equal(c, ref[1]) and torch.equal(d, ref[2])
     top = (ref[0].view(torch.int32) >> 16).to(torch.int16)
     assert torch.equal(h, top)
-
-
-@pytest.mark.slow
-def test_mistral7b_shard16_full_size():
-    """The benchmark workload at full size and in the benchmark's launch
-    configuration: the 453,001,472-element 1/16 shard of Mistral-7B at rank
-    15 (indices beyond 2^32), warm state at step 5.  Digest and bf16 digest
-    against the oracle over host threads, and every output bitwise."""
-    import torch
-
-    pk = _pk()
-    w = wl.WORKLOADS["mistral7b_shard16"]
-    print(f"[{w.name}] drawing {w.numel} elements", flush=True)
-    p, g, m, v = wl.arrays_host(w)
-    sh = make_shard(p, g, m, v, w.global_offset)
-    print(f"[{w.name}] GPU commit", flush=True)
-    d_gpu = pk.to_u64(pk.adamw_commit(sh, w.first_step, g_hyper(H)))[0]
-    bd_gpu = pk.to_u64(pk.bf16_digest(sh))[0]
-    print(f"[{w.name}] oracle commit", flush=True)
-    b = np.zeros(p.size, np.uint16)
-    d_ref = oracle_commit_parallel(p, g, m, v, b, o_hyper(H), w.first_step, w.global_offset)
-    assert d_gpu == d_ref
-    assert bd_gpu == oracle.bf16_digest(b, w.global_offset)
-    _compare_full(sh, p, m, v, b)
-    assert pk.to_u64(pk.shard_digest(sh))[0] == oracle_digest_parallel(p, m, v, w.global_offset)
-    del torch
