@@ -47,6 +47,11 @@ def parse():
                     help="target seconds for each CPU oracle leg (single thread, all threads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--layout", choices=("spread", "packed"), default="spread",
+                    help="spread: the five arrays in one ShardArena pool, each in its own region of HBM "
+                         "(the library's recommended placement); packed: five separate allocations")
+    ap.add_argument("--no-compare-layout", action="store_true",
+                    help="skip timing the other layout as well")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) of a "
                          "bench run into profiles/traffic_<workload>.json and exit")
@@ -203,54 +208,52 @@ def main():
         hypers = [pk.Hyper(**h) for h in w.hypers]
     else:
         segments, hypers = None, None
+    hyper = None if segments else pk.Hyper(**w.hypers[0])
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     n = w.numel
-    t_setup = time.perf_counter()
-    tensors = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(4)]
-    for t, aid, step, dist in zip(tensors, (wl.ARRAY_PARAM, wl.ARRAY_GRAD, wl.ARRAY_EXP_AVG, wl.ARRAY_EXP_AVG_SQ),
-                                  (0, w.first_step, 0, 0), (w.param, w.grad, w.exp_avg, w.exp_avg_sq)):
-        wl.fill_device(t, w.global_offset, w.seed, aid, step, dist)
-    bf16 = torch.zeros(n, dtype=torch.int16, device=dev)
-    sh = pk.Shard(*tensors, bf16, global_offset=w.global_offset, segments=segments, hypers=hypers)
-    hyper = None if segments else pk.Hyper(**w.hypers[0])
-    setup_s = time.perf_counter() - t_setup
-    print(f"[bench] {w.name}: {n} elements resident ({setup_s:.1f} s setup)", file=sys.stderr, flush=True)
-
-    step = w.first_step
-    for _ in range(args.warmup):
-        pk.adamw_commit(sh, step, hyper)
-        step += 1
-    torch.cuda.synchronize()
-
-    K = args.steps
-    ev_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    region_s, region_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    region_s.record()
-    for k in range(K):
-        ev_s[k].record()
-        pk.adamw_commit(sh, step, hyper)
-        ev_e[k].record()
-        step += 1
-    region_e.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = region_s.elapsed_time(region_e)
-    per_launch_ms = [a.elapsed_time(b) for a, b in zip(ev_s, ev_e)]
-    last_digest = pk.to_u64(sh.digest)[-1]
-    ms_per_step = total_ms / K
-    avg_launch_ms = sum(per_launch_ms) / K
-    value = n / (ms_per_step / 1e3)
     algo_bytes = BYTES_PER_ELEM * n
-    achieved = algo_bytes / (avg_launch_ms / 1e3) / 1e9
-    print(f"[bench] {K} commits: {ms_per_step:.4f} ms/step, kernel {avg_launch_ms:.4f} ms avg "
-          f"(min {min(per_launch_ms):.4f}), {achieved:.1f} GB/s", file=sys.stderr, flush=True)
 
-    probe = None
-    if not args.no_probe and segments is None:
+    def allocate(layout):
+        if layout == "spread":
+            arena = pk.ShardArena(n, dev)
+            return arena, [arena.param, arena.grad, arena.exp_avg, arena.exp_avg_sq], arena.param_bf16
+        ts = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(4)]
+        return None, ts, torch.empty(n, dtype=torch.int16, device=dev)
+
+    def fill(tensors, bf16):
+        for t, aid, st, dist in zip(tensors, (wl.ARRAY_PARAM, wl.ARRAY_GRAD, wl.ARRAY_EXP_AVG, wl.ARRAY_EXP_AVG_SQ),
+                                    (0, w.first_step, 0, 0), (w.param, w.grad, w.exp_avg, w.exp_avg_sq)):
+            wl.fill_device(t, w.global_offset, w.seed, aid, st, dist)
+        bf16.zero_()
+
+    def measure(sh, K, W):
+        """W untimed commits, then K timed ones; hipEvents around each call and
+        around the whole timed region, on the stream the library launches on."""
+        step = w.first_step
+        for _ in range(W):
+            pk.adamw_commit(sh, step, hyper)
+            step += 1
+        torch.cuda.synchronize()
+        ev_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+        ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+        region_s, region_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        region_s.record()
+        for k in range(K):
+            ev_s[k].record()
+            pk.adamw_commit(sh, step, hyper)
+            ev_e[k].record()
+            step += 1
+        region_e.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        per_launch = [a.elapsed_time(b) for a, b in zip(ev_s, ev_e)]
+        return {"ms_per_step": region_s.elapsed_time(region_e) / K, "avg_launch_ms": sum(per_launch) / K,
+                "min_launch_ms": min(per_launch), "wall_s": wall, "digest": pk.to_u64(sh.digest)[-1]}
+
+    def probe(tensors, bf16, K):
         p_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
         p_e = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
         for k in range(K):
@@ -259,10 +262,57 @@ def main():
             p_e[k].record()
         torch.cuda.synchronize()
         pms = sum(a.elapsed_time(b) for a, b in zip(p_s, p_e)) / K
-        probe = {"kernel": "stream_probe", "ms": pms, "gbps": algo_bytes / (pms / 1e3) / 1e9,
-                 "frac_of_peak": algo_bytes / (pms / 1e3) / 1e9 / PEAK_HBM_GBPS}
-        print(f"[bench] stream probe (same 30 B/element, no math): {probe['gbps']:.1f} GB/s",
+        return {"kernel": "stream_probe", "ms": pms, "gbps": algo_bytes / (pms / 1e3) / 1e9,
+                "frac_of_peak": algo_bytes / (pms / 1e3) / 1e9 / PEAK_HBM_GBPS}
+
+    t_setup = time.perf_counter()
+    arena, tensors, bf16 = allocate(args.layout)
+    fill(tensors, bf16)
+    sh = pk.Shard(*tensors, bf16, global_offset=w.global_offset, segments=segments, hypers=hypers)
+    setup_s = time.perf_counter() - t_setup
+    print(f"[bench] {w.name}: {n} elements resident, {args.layout} layout ({setup_s:.1f} s setup)",
+          file=sys.stderr, flush=True)
+
+    K = args.steps
+    main_m = measure(sh, K, args.warmup)
+    ms_per_step = main_m["ms_per_step"]
+    avg_launch_ms = main_m["avg_launch_ms"]
+    value = n / (ms_per_step / 1e3)
+    achieved = algo_bytes / (avg_launch_ms / 1e3) / 1e9
+    print(f"[bench] {K} commits: {ms_per_step:.4f} ms/step, kernel {avg_launch_ms:.4f} ms avg "
+          f"(min {main_m['min_launch_ms']:.4f}), {achieved:.1f} GB/s", file=sys.stderr, flush=True)
+    last_digest = main_m["digest"]
+    wall = main_m["wall_s"]
+
+    probe_res = None
+    if not args.no_probe and segments is None:
+        probe_res = probe(tensors, bf16, K)
+        print(f"[bench] stream probe (same 30 B/element, no math): {probe_res['gbps']:.1f} GB/s",
               file=sys.stderr, flush=True)
+
+    other = None
+    if not args.no_compare_layout:
+        other_layout = "packed" if args.layout == "spread" else "spread"
+        del sh
+        free, _ = torch.cuda.mem_get_info(dev)
+        need = 4 * n * 4 + 2 * n if other_layout == "packed" else 4 * (40 << 30) + 2 * n
+        if free > need + (2 << 30):
+            o_arena, o_t, o_b = allocate(other_layout)
+            fill(o_t, o_b)
+            o_sh = pk.Shard(*o_t, o_b, global_offset=w.global_offset, segments=segments, hypers=hypers)
+            om = measure(o_sh, K, args.warmup)
+            other = {"layout": other_layout, "ms_per_step": om["ms_per_step"],
+                     "value": n / (om["ms_per_step"] / 1e3),
+                     "achieved_gbps": algo_bytes / (om["avg_launch_ms"] / 1e3) / 1e9,
+                     "frac": algo_bytes / (om["avg_launch_ms"] / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                     "same_digest": om["digest"] == last_digest}
+            if segments is None and not args.no_probe:
+                other["probe_gbps"] = probe(o_t, o_b, K)["gbps"]
+            print(f"[bench] {other_layout} layout: {om['ms_per_step']:.4f} ms/step, "
+                  f"{other['achieved_gbps']:.1f} GB/s", file=sys.stderr, flush=True)
+            del o_sh, o_t, o_b, o_arena
+        else:
+            print(f"[bench] {other_layout} layout skipped: not enough free device memory", file=sys.stderr)
 
     src_hash = kernel_source_hash()
     traffic_rec = stored_traffic(w.name, src_hash)
@@ -287,12 +337,14 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Philox4x32-10 inputs with the workload's shapes and distributions)",
         "config": dict(w.describe(), parallelism="one rank's shard, no collectives",
-                       bytes_per_element=BYTES_PER_ELEM),
+                       bytes_per_element=BYTES_PER_ELEM,
+                       layout=("spread: the five arrays in one ShardArena pool, 40 GiB apart"
+                               if args.layout == "spread" else "packed: five separate torch allocations")),
         "hbm_gbps_nominal": algo_bytes / (ms_per_step / 1e3) / 1e9,
         "pct_of_peak_hbm": 100.0 * algo_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,
         "roofline": {
             "bound": "hbm",
-            "kernel": "shard_kernel<Commit>",
+            "kernel": "tile_kernel<Commit>",
             "achieved": achieved,
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
@@ -300,11 +352,12 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": algo_bytes,
             "avg_launch_ms": avg_launch_ms,
-            "timing": "hipEvents around each commit call on the launch stream (includes the digest-slot "
-                      "zeroing kernel, about 2 us)",
+            "timing": "hipEvents around each commit call on the launch stream; a call also runs the "
+                      "one-workgroup kernels that clear and sum the digest lanes (a few microseconds)",
         },
         "cpu_baseline": cpu,
-        "probe": probe,
+        "probe": probe_res,
+        "other_layout": other,
         "kernel_source_hash": src_hash,
         "last_digest": f"{last_digest:#018x}",
         "wall_s_timed_region": wall,

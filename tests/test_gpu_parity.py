@@ -354,3 +354,31 @@ def test_stream_probe_moves_the_bytes():
     assert torch.equal(a, ref[0]) and torch.equal(c, ref[1]) and torch.equal(d, ref[2])
     top = (ref[0].view(torch.int32) >> 16).to(torch.int16)
     assert torch.equal(h, top)
+
+
+def test_shard_arena_layout():
+    """The placement-aware arena: five arrays at `spacing` strides in one
+    pool, gaps usable through take(), and a commit on it equal to the oracle."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["decoder1b_shard16"]
+    n = 3 * 4096 + 17
+    arena = pk.ShardArena(n, "cuda", spacing=64 << 20)
+    base = arena.pool.data_ptr()
+    ptrs = [t.data_ptr() - base for t in (arena.param, arena.grad, arena.exp_avg, arena.exp_avg_sq, arena.param_bf16)]
+    assert ptrs == [k * (64 << 20) for k in range(5)]
+    extra = arena.take(1 << 20, torch.float32)
+    assert extra.numel() == (1 << 18) and extra.data_ptr() - base >= n * 4
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    for t, a in zip((arena.param, arena.grad, arena.exp_avg, arena.exp_avg_sq), (p, g, m, v)):
+        t.copy_(torch.from_numpy(a))
+    extra.fill_(7.0)
+    sh = arena.shard(w.global_offset)
+    d = pk.to_u64(pk.adamw_commit(sh, 100, g_hyper(H)))[0]
+    b = np.zeros(n, np.uint16)
+    assert d == oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), 100, w.global_offset)
+    _compare_full(sh, p, m, v, b)
+    assert bool((extra == 7.0).all())
+    with pytest.raises(MemoryError):
+        arena.take(1 << 30)
