@@ -382,3 +382,30 @@ def test_shard_arena_layout():
     assert bool((extra == 7.0).all())
     with pytest.raises(MemoryError):
         arena.take(1 << 30)
+
+
+def test_stored_oracle_digests():
+    """The library reproduces the digests the oracle stored in tests/golden/."""
+    import json
+    import os
+
+    import torch
+
+    pk = _pk()
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_digests.json")
+    for c in json.load(open(path)):
+        if c["workload"] == "shrunken_mistral":
+            w = wl.shrunken_mistral()
+            p, g, m, v = wl.arrays_host(w)
+            sh = make_shard(p, g, m, v, w.global_offset, segments=w.segments, hypers=w.hypers)
+            got = pk.to_u64(pk.adamw_commit(sh, c["step"]))
+            assert [f"{x:#018x}" for x in got[:-1]] == c["segment_digests"]
+            total = got[-1]
+        else:
+            w = wl.WORKLOADS[c["workload"]]
+            p, g, m, v = wl.arrays_host(w, c["start"], c["count"])
+            sh = make_shard(p, g, m, v, w.global_offset + c["start"])
+            total = pk.to_u64(pk.adamw_commit(sh, c["step"], g_hyper(w.hypers[0])))[0]
+        assert f"{total:#018x}" == c["state_digest"], c["name"]
+        assert f"{pk.to_u64(pk.bf16_digest(sh))[-1]:#018x}" == c["bf16_digest"], c["name"]
+        del torch
