@@ -290,6 +290,38 @@ def main():
         print(f"[bench] stream probe (same 30 B/element, no math): {probe_res['gbps']:.1f} GB/s",
               file=sys.stderr, flush=True)
 
+    # the neighbouring kernels on the same shard (after the timed region):
+    # the commit that also zeroes the gradient (34 B/element), the gradient
+    # guard (4 B/element) and the standalone state digest (12 B/element)
+    extra = {}
+    if not args.no_probe:
+        def time_call(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s_ev.record()
+            for _ in range(reps):
+                fn()
+            e_ev.record()
+            torch.cuda.synchronize()
+            return s_ev.elapsed_time(e_ev) / reps
+
+        reps = max(3, K // 2)
+        zstep = [w.first_step + args.warmup + K]
+
+        def zcommit():
+            pk.adamw_commit(sh, zstep[0], hyper, zero_grad=True)
+            zstep[0] += 1
+
+        for name, fn, bpe in (("commit_zero_grad", zcommit, 34),
+                              ("grad_guard", lambda: pk.grad_guard(sh), 4),
+                              ("shard_digest", lambda: pk.shard_digest(sh), 12)):
+            ms = time_call(fn, reps)
+            extra[name] = {"ms": ms, "bytes_per_element": bpe, "gbps": bpe * n / (ms / 1e3) / 1e9,
+                           "frac_of_peak": bpe * n / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS}
+            print(f"[bench] {name}: {ms:.4f} ms, {extra[name]['gbps']:.1f} GB/s at {bpe} B/element",
+                  file=sys.stderr, flush=True)
+
     other = None
     if not args.no_compare_layout:
         other_layout = "packed" if args.layout == "spread" else "spread"
@@ -358,6 +390,7 @@ def main():
         "cpu_baseline": cpu,
         "probe": probe_res,
         "other_layout": other,
+        "other_kernels": extra,
         "kernel_source_hash": src_hash,
         "last_digest": f"{last_digest:#018x}",
         "wall_s_timed_region": wall,

@@ -136,6 +136,26 @@ int64_t pact_workspace_bytes(const pact_shard* s);
  * step = the optimizer step t >= 1 after its increment. */
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper);
 
+/* Options of pact_adamw_commit_ex. */
+#define PACT_COMMIT_ZERO_GRAD 1u /* the same pass writes +0.0 into every committed grad element */
+
+/* The commit with options; flags = 0 is exactly pact_adamw_commit.
+ * PACT_COMMIT_ZERO_GRAD: after reading g, the same pass writes +0.0 into
+ * every committed element of `grad` (4 more bytes per element, 34 in all),
+ * so that one call leaves the shard at the boundary the paper admits for
+ * in-memory recovery: update committed and flat gradients zeroed (Sec. I;
+ * Sec. III-C, phase 2).  `grad` must then be writable device memory (the
+ * const in pact_shard does not hold for this call).  Unknown flag bits are
+ * PACT_EINVAL. */
+int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags);
+
+/* Boundary guard for zero outstanding gradients (Sec. III-C, phase 2):
+ * counts the elements of `grad` whose 32-bit pattern is not all zero (-0.0
+ * counts as outstanding), per segment and in total, into dev_out
+ * (pact_digest_slots() uint64 slots, device memory).  param, exp_avg,
+ * exp_avg_sq and param_bf16 are not read and may be NULL. */
+int pact_grad_guard(const pact_shard* s, uint64_t* dev_out);
+
 /* Digest of the current (p, m, v) without updating them (the bitwise state
  * check of Sec. IV-G, as a 64-bit identity).  grad and param_bf16 are not
  * read and may be NULL. */

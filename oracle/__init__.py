@@ -96,6 +96,10 @@ def _load():
             f32p, f32p, f32p, f32p, u16p, u64, u64, ctypes.POINTER(_Hyper), u64,
         ]
         lib.oracle_commit_and_digest.restype = u64
+        lib.oracle_zero_grad.argtypes = [f32p, u64]
+        lib.oracle_zero_grad.restype = None
+        lib.oracle_count_outstanding.argtypes = [f32p, u64]
+        lib.oracle_count_outstanding.restype = u64
         _lib = lib
     return _lib
 
@@ -194,6 +198,18 @@ def commit_and_digest(p, g, m, v, bf16, h: Hyper, step: int, first_index: int) -
             ctypes.byref(_hyper(h)), step,
         )
     )
+
+
+def zero_grad(g) -> None:
+    """The gradient at the committed boundary: every element +0.0."""
+    _check(g, np.float32, "g")
+    _load().oracle_zero_grad(_ptr(g, ctypes.c_float), g.size)
+
+
+def count_outstanding(g) -> int:
+    """Gradient elements whose bit pattern is not all zero."""
+    _check(g, np.float32, "g")
+    return int(_load().oracle_count_outstanding(_ptr(g, ctypes.c_float), g.size))
 
 
 def commit_segments(p, g, m, v, bf16, segments: Sequence[tuple[int, int, int]],

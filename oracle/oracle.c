@@ -174,3 +174,23 @@ uint64_t oracle_commit_and_digest(float* p, const float* g, float* m, float* v,
     oracle_adamw_commit(p, g, m, v, bf16, n, &sc);
     return oracle_state_digest(p, m, v, n, first_index);
 }
+
+/* ------------------------------------------------------------------------ */
+/* The quiescent boundary: gradients zeroed once the update has committed     */
+/* (Sec. I; Sec. III-C, phase 2), and the guard that checks it.              */
+/* ------------------------------------------------------------------------ */
+void oracle_zero_grad(float* g, uint64_t n) {
+    for (uint64_t i = 0; i < n; i++) {
+        g[i] = 0.0f;
+    }
+}
+
+uint64_t oracle_count_outstanding(const float* g, uint64_t n) {
+    uint64_t count = 0;
+    for (uint64_t i = 0; i < n; i++) {
+        if (f32_bits(g[i]) != 0u) {
+            count++;
+        }
+    }
+    return count;
+}

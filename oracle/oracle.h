@@ -79,6 +79,14 @@ uint64_t oracle_state_digest(const float* p, const float* m, const float* v,
 /* Digest of the bf16 copy, tag 3, 16-bit words zero-extended. */
 uint64_t oracle_bf16_digest(const uint16_t* b, uint64_t n, uint64_t first_index);
 
+/* The committed boundary also has the flat gradients zeroed (Sec. I;
+ * Sec. III-C, phase 2): every element of g becomes +0.0. */
+void oracle_zero_grad(float* g, uint64_t n);
+
+/* Boundary guard: gradient elements whose 32-bit pattern is not all zero
+ * (an outstanding gradient; -0.0 counts). */
+uint64_t oracle_count_outstanding(const float* g, uint64_t n);
+
 /* Commit followed by the digest of the committed state: the whole hot path. */
 uint64_t oracle_commit_and_digest(float* p, const float* g, float* m, float* v,
                                   uint16_t* bf16, uint64_t n, uint64_t first_index,

@@ -23,7 +23,8 @@ from typing import Optional, Sequence, Tuple
 import torch
 
 __all__ = [
-    "Hyper", "Shard", "ShardArena", "PactError", "adamw_commit", "shard_digest", "bf16_digest", "stream_probe",
+    "Hyper", "Shard", "ShardArena", "PactError", "adamw_commit", "grad_guard", "shard_digest", "bf16_digest",
+    "stream_probe",
     "digest_slots", "to_u64", "library_path",
 ]
 
@@ -77,6 +78,10 @@ def _lib():
         P = ctypes.POINTER(_CShard)
         lib.pact_adamw_commit.argtypes = [P, ctypes.c_uint64, ctypes.POINTER(_CHyper)]
         lib.pact_adamw_commit.restype = ctypes.c_int
+        lib.pact_adamw_commit_ex.argtypes = [P, ctypes.c_uint64, ctypes.POINTER(_CHyper), ctypes.c_uint32]
+        lib.pact_adamw_commit_ex.restype = ctypes.c_int
+        lib.pact_grad_guard.argtypes = [P, ctypes.c_void_p]
+        lib.pact_grad_guard.restype = ctypes.c_int
         lib.pact_shard_digest.argtypes = [P]
         lib.pact_shard_digest.restype = ctypes.c_int
         lib.pact_bf16_digest.argtypes = [P, ctypes.c_void_p]
@@ -251,8 +256,12 @@ def digest_slots(shard: Shard) -> int:
     return int(_lib().pact_digest_slots(ctypes.byref(shard._c())))
 
 
-def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None) -> torch.Tensor:
-    """Commit one AdamW step on the shard (in place) and digest the result.
+PACT_COMMIT_ZERO_GRAD = 1
+
+
+def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None, zero_grad: bool = False) -> torch.Tensor:
+    """Commit one AdamW step on the shard (in place) and digest the result;
+    with ``zero_grad`` the same pass also writes +0.0 into the gradient.
 
     Returns the device tensor of digest slots (int64 holding uint64 bits); it
     holds the values once the current stream reaches this point.
@@ -260,11 +269,22 @@ def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None) -> torc
     if shard.segments is None and hyper is None:
         hyper = Hyper()
     ch = hyper._c() if hyper is not None else None
+    flags = PACT_COMMIT_ZERO_GRAD if zero_grad else 0
     with torch.cuda.device(shard.device):
-        rc = _lib().pact_adamw_commit(ctypes.byref(shard._c()), int(step),
-                                      ctypes.byref(ch) if ch is not None else None)
-    _call("pact_adamw_commit", rc)
+        rc = _lib().pact_adamw_commit_ex(ctypes.byref(shard._c()), int(step),
+                                         ctypes.byref(ch) if ch is not None else None, flags)
+    _call("pact_adamw_commit_ex", rc)
     return shard.digest
+
+
+def grad_guard(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Count the gradient elements that are not +0.0 (per segment and total)."""
+    if out is None:
+        out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_grad_guard(ctypes.byref(shard._c()), out.data_ptr())
+    _call("pact_grad_guard", rc)
+    return out
 
 
 def shard_digest(shard: Shard) -> torch.Tensor:

@@ -1,6 +1,7 @@
 // kernels.hip -- gfx950 kernels of libpactshard.
 //
-// One tile kernel serves the three modes (commit, state digest, bf16 digest).
+// One tile kernel serves every mode (commit, commit that also zeroes the
+// gradient, state digest, bf16 digest, gradient guard).
 // Work is cut into tiles of kTile elements that never straddle a segment, and
 // each workgroup takes exactly one tile (the hardware dispatcher then keeps
 // every CU full and balances the tail by itself; a persistent grid measured
@@ -142,20 +143,28 @@ __device__ __forceinline__ void store8(u32x2 x, __amdgpu_buffer_rsrc_t r, uint32
 // one element, element-wise path (ragged tails, misaligned segments)
 // ---------------------------------------------------------------------------
 template <Mode M>
+constexpr bool kCommits = (M == Mode::Commit || M == Mode::CommitZeroGrad);
+
+template <Mode M>
 __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const StepScalars& sc) {
     const uint64_t idx = a.goff + e;
     if constexpr (M == Mode::Bf16Digest) {
         return hash_word(a.b[e], idx | kTagB);
+    } else if constexpr (M == Mode::GradGuard) {
+        return __float_as_uint(a.g[e]) != 0u ? 1u : 0u;
     } else {
         float p = a.p[e];
         float m = a.m[e];
         float v = a.v[e];
-        if constexpr (M == Mode::Commit) {
+        if constexpr (kCommits<M>) {
             adamw(p, a.g[e], m, v, sc);
             a.p[e] = p;
             a.m[e] = m;
             a.v[e] = v;
             a.b[e] = (uint16_t)to_bf16(p);
+            if constexpr (M == Mode::CommitZeroGrad) {
+                a.g_zero[e] = 0.0f;
+            }
         }
         return hash_word(__float_as_uint(p), idx) + hash_word(__float_as_uint(m), idx | kTagM) +
                hash_word(__float_as_uint(v), idx | kTagV);
@@ -175,7 +184,22 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
     const uint32_t lane16 = threadIdx.x * kVec * 2;
     const uint64_t lane_idx = a.goff + e0 + threadIdx.x * kVec;
     uint64_t acc = 0;
-    if constexpr (M == Mode::Bf16Digest) {
+    if constexpr (M == Mode::GradGuard) {
+        const auto rg = tile_rsrc(a.g + e0, kTile * 4);
+        u32x4 G[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            G[u] = load16(rg, lane32 + u * kRow32);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+            for (int j = 0; j < kVec; ++j) {
+                acc += G[u][j] != 0u ? 1u : 0u;
+            }
+        }
+        return acc;
+    } else if constexpr (M == Mode::Bf16Digest) {
         const auto rb = tile_rsrc(a.b + e0, kTile * 2);
         u32x2 W[kUnroll];
 #pragma unroll
@@ -200,11 +224,18 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
             Mo[u] = load16(rm, lane32 + u * kRow32);
             V[u] = load16(rv, lane32 + u * kRow32);
         }
-        if constexpr (M == Mode::Commit) {
+        if constexpr (kCommits<M>) {
             const auto rg = tile_rsrc(a.g + e0, kTile * 4);
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 G[u] = load16(rg, lane32 + u * kRow32);
+            }
+            if constexpr (M == Mode::CommitZeroGrad) {
+                const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    store16(zero, rg, lane32 + u * kRow32);
+                }
             }
             const auto rb = tile_rsrc(a.b + e0, kTile * 2);
 #pragma unroll
@@ -383,6 +414,12 @@ hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t gri
             break;
         case Mode::Bf16Digest:
             hipLaunchKernelGGL(tile_kernel<Mode::Bf16Digest>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            break;
+        case Mode::CommitZeroGrad:
+            hipLaunchKernelGGL(tile_kernel<Mode::CommitZeroGrad>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            break;
+        case Mode::GradGuard:
+            hipLaunchKernelGGL(tile_kernel<Mode::GradGuard>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
     }
     return hipGetLastError();

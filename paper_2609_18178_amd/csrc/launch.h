@@ -45,6 +45,7 @@ struct Batch {
 struct Arrays {
     float* p;
     const float* g;
+    float* g_zero;      // the grad array, written only by Mode::CommitZeroGrad
     float* m;
     float* v;
     uint16_t* b;
@@ -53,7 +54,7 @@ struct Arrays {
     uint64_t* lanes;    // workspace lanes, or null: atomics go to the result slots
 };
 
-enum class Mode : int { Commit = 0, StateDigest = 1, Bf16Digest = 2 };
+enum class Mode : int { Commit = 0, StateDigest = 1, Bf16Digest = 2, CommitZeroGrad = 3, GradGuard = 4 };
 
 // Enqueue the clearing of what the tile kernels accumulate into: the
 // nres * kLanes lane words when `lanes` is given, else the nslots digest slots.

@@ -167,6 +167,7 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
     pact::Arrays a;
     a.p = s->param;
     a.g = s->grad;
+    a.g_zero = const_cast<float*>(s->grad);  // written only by Mode::CommitZeroGrad
     a.m = s->exp_avg;
     a.v = s->exp_avg_sq;
     a.b = s->param_bf16;
@@ -191,13 +192,15 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
             b.elem_count[k] = w.count;
             b.sc[k] = w.sc;
             bool ok = true;
-            if (mode != pact::Mode::Bf16Digest) {
+            if (mode == pact::Mode::Bf16Digest) {
+                ok = aligned(a.b + w.first, 8);
+            } else if (mode == pact::Mode::GradGuard) {
+                ok = aligned(a.g + w.first, 16);
+            } else {
                 ok = aligned(a.p + w.first, 16) && aligned(a.m + w.first, 16) && aligned(a.v + w.first, 16);
-                if (mode == pact::Mode::Commit) {
+                if (mode == pact::Mode::Commit || mode == pact::Mode::CommitZeroGrad) {
                     ok = ok && aligned(a.g + w.first, 16) && aligned(a.b + w.first, 8);
                 }
-            } else {
-                ok = aligned(a.b + w.first, 8);
             }
             b.vec_ok[k] = ok ? 1u : 0u;
         }
@@ -257,15 +260,30 @@ int64_t pact_workspace_bytes(const pact_shard* s) {
     return (int64_t)workspace_need(s);
 }
 
-int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
-    if (s == nullptr || step == 0) return PACT_EINVAL;
+int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags) {
+    if (s == nullptr || step == 0 || (flags & ~PACT_COMMIT_ZERO_GRAD) != 0) return PACT_EINVAL;
     if (s->segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
     uint64_t nslots = 0;
     int rc = validate(s, Uses{true, true, true, true, true}, s->digest_dev, &nslots);
     if (rc != PACT_OK) return rc;
     std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
     if (rc != PACT_OK) return rc;
-    return run(pact::Mode::Commit, s, work, s->digest_dev, nslots);
+    const pact::Mode mode = (flags & PACT_COMMIT_ZERO_GRAD) ? pact::Mode::CommitZeroGrad : pact::Mode::Commit;
+    return run(mode, s, work, s->digest_dev, nslots);
+}
+
+int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
+    return pact_adamw_commit_ex(s, step, hyper, 0u);
+}
+
+int pact_grad_guard(const pact_shard* s, uint64_t* dev_out) {
+    if (s == nullptr) return PACT_EINVAL;
+    uint64_t nslots = 0;
+    int rc = validate(s, Uses{false, true, false, false, false}, dev_out, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(pact::Mode::GradGuard, s, work, dev_out, nslots);
 }
 
 int pact_shard_digest(const pact_shard* s) {

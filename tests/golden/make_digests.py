@@ -40,9 +40,10 @@ def cases():
     b = np.zeros(p.size, np.uint16)
     per, total = oracle.commit_segments(p, g, m, v, b, w.segments, [oracle.Hyper(**h) for h in w.hypers],
                                         w.first_step, w.global_offset)
+    # padding is not digested: the bf16 digest is the sum over segments
+    bf = sum(oracle.bf16_digest(b[o:o + ln], w.global_offset + o) for o, ln, _ in w.segments) & oracle.MASK64
     out.append(dict(name="mistral_shrunk", workload="shrunken_mistral", start=0, count=w.numel,
-                    step=w.first_step, segment_digests=per, state_digest=total,
-                    bf16_digest=oracle.bf16_digest(b, w.global_offset)))
+                    step=w.first_step, segment_digests=per, state_digest=total, bf16_digest=bf))
     return out
 
 

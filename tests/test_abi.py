@@ -141,6 +141,20 @@ def test_digest_slots():
     assert commit(s, h=None) == pk.PACT_EOVERLAP
 
 
+def test_commit_ex_and_guard_validation():
+    lib = pk._lib()
+    s = fake_shard()
+    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 1, ctypes.byref(GOOD), 2) == pk.PACT_EINVAL
+    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 0, ctypes.byref(GOOD), 1) == pk.PACT_EINVAL
+    assert lib.pact_adamw_commit_ex(ctypes.byref(fake_shard(grad=BASE)), 1, ctypes.byref(GOOD), 1) == \
+        pk.PACT_EOVERLAP
+    assert lib.pact_grad_guard(None, BASE + 7 * SPAN) == pk.PACT_EINVAL
+    assert lib.pact_grad_guard(ctypes.byref(fake_shard(grad=None)), BASE + 7 * SPAN) == pk.PACT_EINVAL
+    assert lib.pact_grad_guard(ctypes.byref(fake_shard()), None) == pk.PACT_EINVAL
+    assert lib.pact_grad_guard(ctypes.byref(fake_shard()), BASE + 7 * SPAN + 4) == pk.PACT_EALIGN
+    assert lib.pact_grad_guard(ctypes.byref(fake_shard()), BASE + SPAN + 8) == pk.PACT_EOVERLAP
+
+
 def test_workspace_contract():
     lib = pk._lib()
     s = fake_shard()

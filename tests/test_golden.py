@@ -50,11 +50,13 @@ def test_oracle_still_reproduces_its_stored_digests():
             per, total = oracle.commit_segments(p, g, m, v, b, w.segments, [oracle.Hyper(**h) for h in w.hypers],
                                                 c["step"], w.global_offset)
             assert [f"{x:#018x}" for x in per] == c["segment_digests"]
+            bf = sum(oracle.bf16_digest(b[o:o + ln], w.global_offset + o) for o, ln, _ in w.segments)
         else:
             w = wl.WORKLOADS[c["workload"]]
             p, g, m, v = wl.arrays_host(w, c["start"], c["count"])
             b = np.zeros(p.size, np.uint16)
             total = oracle.commit_and_digest(p, g, m, v, b, oracle.Hyper(**w.hypers[0]), c["step"],
                                              w.global_offset + c["start"])
+            bf = oracle.bf16_digest(b, w.global_offset + c["start"])
         assert f"{total:#018x}" == c["state_digest"], c["name"]
-        assert f"{oracle.bf16_digest(b, w.global_offset + c['start']):#018x}" == c["bf16_digest"], c["name"]
+        assert f"{bf & oracle.MASK64:#018x}" == c["bf16_digest"], c["name"]

@@ -389,8 +389,6 @@ def test_stored_oracle_digests():
     import json
     import os
 
-    import torch
-
     pk = _pk()
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_digests.json")
     for c in json.load(open(path)):
@@ -408,4 +406,46 @@ def test_stored_oracle_digests():
             total = pk.to_u64(pk.adamw_commit(sh, c["step"], g_hyper(w.hypers[0])))[0]
         assert f"{total:#018x}" == c["state_digest"], c["name"]
         assert f"{pk.to_u64(pk.bf16_digest(sh))[-1]:#018x}" == c["bf16_digest"], c["name"]
-        del torch
+
+
+@pytest.mark.parametrize("segmented", [False, True])
+def test_commit_zero_grad_and_guard(segmented):
+    """The commit that also zeroes the gradient leaves the committed boundary
+    (update applied, gradients +0.0): every output equals the oracle's, the
+    guard counts the outstanding gradients before (as numpy does) and none
+    after, per segment; padding in the gradient is untouched."""
+    import torch
+
+    pk = _pk()
+    w = wl.shrunken_mistral() if segmented else wl.WORKLOADS["decoder1b_shard16"]
+    n = w.numel if segmented else 100003
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    g[::97] = 0.0
+    g[1::101] = -0.0
+    segs = w.segments if segmented else [(0, n, 0)]
+    sh = make_shard(p, g, m, v, w.global_offset, segments=w.segments if segmented else None,
+                    hypers=w.hypers if segmented else None)
+    before = pk.to_u64(pk.grad_guard(sh))
+    want_before = [oracle.count_outstanding(g[o:o + ln].copy()) for o, ln, _ in segs]
+    assert before[:len(want_before)] == want_before
+    assert before[-1] == sum(want_before)
+    hy = None if segmented else g_hyper(H)
+    got = pk.to_u64(pk.adamw_commit(sh, w.first_step, hy, zero_grad=True))
+    b = np.zeros(n, np.uint16)
+    g_ref = g.copy()
+    per = []
+    for o, ln, hi in segs:
+        sl = slice(o, o + ln)
+        hyper = o_hyper(w.hypers[hi]) if segmented else o_hyper(H)
+        per.append(oracle.commit_and_digest(p[sl], g[sl], m[sl], v[sl], b[sl], hyper, w.first_step,
+                                            w.global_offset + o))
+        gz = g_ref[sl].copy()
+        oracle.zero_grad(gz)
+        g_ref[sl] = gz
+    want = per + [sum(per) & M64] if segmented else [per[0]]
+    assert got == want
+    _compare_full(sh, p, m, v, b)
+    assert_bitwise("grad", host(sh.grad), g_ref)
+    after = pk.to_u64(pk.grad_guard(sh))
+    assert after == [0] * len(after)
+    del torch

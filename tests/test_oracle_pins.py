@@ -413,3 +413,20 @@ def test_mistral_shape_arithmetic():
     assert wl.MISTRAL_SHARD4 == 1_812_005_888
     per_layer = sum(n for name, n, _ in t if name.startswith("model.layers.0."))
     assert per_layer == 218_112_000
+
+
+# ---------------------------------------------------------------------------
+# committed boundary: zeroed gradients and the guard
+# ---------------------------------------------------------------------------
+
+def test_guard_counts_nonzero_bit_patterns():
+    """Library routine: numpy's count_nonzero over the bit patterns; -0.0 and
+    denormals count as outstanding, +0.0 does not."""
+    rng = np.random.default_rng(10)
+    g = rng.standard_normal(100003).astype(np.float32)
+    g[rng.integers(0, g.size, 5000)] = 0.0
+    g[:7] = [-0.0, 0.0, 1e-45, -1e-45, np.inf, 0.0, -0.0]
+    assert oracle.count_outstanding(g) == int(np.count_nonzero(g.view(np.uint32)))
+    oracle.zero_grad(g)
+    assert not g.view(np.uint32).any() and oracle.count_outstanding(g) == 0
+    assert oracle.count_outstanding(np.zeros(0, np.float32)) == 0
