@@ -313,9 +313,26 @@ def main():
             pk.adamw_commit(sh, zstep[0], hyper, zero_grad=True)
             zstep[0] += 1
 
-        for name, fn, bpe in (("commit_zero_grad", zcommit, 34),
-                              ("grad_guard", lambda: pk.grad_guard(sh), 4),
-                              ("shard_digest", lambda: pk.shard_digest(sh), 12)):
+        kernels = [("commit_zero_grad", zcommit, 34), ("grad_guard", lambda: pk.grad_guard(sh), 4),
+                   ("shard_digest", lambda: pk.shard_digest(sh), 12)]
+        # the same shard held in BF16 (the paper's precision), 14 B/element:
+        # its four arrays in four separate regions of the arena when spread
+        if segments is None:
+            b16 = []
+            for k, t in enumerate(tensors):
+                dst = (arena.take(n * 2, torch.int16, region=k) if arena is not None
+                       else torch.empty(n, dtype=torch.int16, device=dev))
+                dst.view(torch.bfloat16).copy_(t)
+                b16.append(dst)
+            sh16 = pk.ShardBf16(*b16, global_offset=w.global_offset)
+            bstep = [w.first_step]
+
+            def bcommit():
+                pk.adamw_commit_bf16(sh16, bstep[0], hyper)
+                bstep[0] += 1
+
+            kernels.append(("commit_bf16_state", bcommit, 14))
+        for name, fn, bpe in kernels:
             ms = time_call(fn, reps)
             extra[name] = {"ms": ms, "bytes_per_element": bpe, "gbps": bpe * n / (ms / 1e3) / 1e9,
                            "frac_of_peak": bpe * n / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS}

@@ -166,6 +166,42 @@ int pact_shard_digest(const pact_shard* s);
  * NULL.  A verification aid: the bf16 copy is a function of p'. */
 int pact_bf16_digest(const pact_shard* s, uint64_t* dev_out);
 
+/* One rank's flat shard held in BF16, the paper's own precision for weights
+ * and AdamW moments (Sec. IV-A): the fields of pact_shard with 16-bit
+ * arrays (bf16 bit patterns) and no separate working copy.  fp32 rules apply
+ * with 2-byte alignment; a segment whose start is 16-byte aligned in all four
+ * arrays runs the vector path. */
+typedef struct pact_shard_bf16 {
+    uint16_t* param;          /* W, bf16, numel elements                       */
+    const uint16_t* grad;     /* bf16 gradient                                 */
+    uint16_t* exp_avg;        /* M, bf16                                       */
+    uint16_t* exp_avg_sq;     /* V, bf16                                       */
+    uint64_t numel;
+    uint64_t global_offset;
+    const pact_segment* segs;
+    uint32_t num_segs;
+    uint32_t num_hypers;
+    const pact_hyper* hypers;
+    uint64_t* digest_dev;
+    void* workspace;
+    uint64_t workspace_bytes;
+    void* stream;
+} pact_shard_bf16;
+
+/* The commit on BF16 state: each bf16 word of p, g, m, v is widened exactly
+ * to binary32, the binary32 update above is applied unchanged, and p', m',
+ * v' are rounded back to bf16 (round to nearest even), in place.  Reads 8 and
+ * writes 6 bytes per element; the digest of (p', m', v') uses the 16-bit
+ * words zero-extended, with the same indices and tags 0, 1, 2. */
+int pact_adamw_commit_bf16(const pact_shard_bf16* s, uint64_t step, const pact_hyper* hyper);
+
+/* Digest of the current BF16 (p, m, v); grad is not read and may be NULL. */
+int pact_shard_digest_bf16(const pact_shard_bf16* s);
+
+/* Slot count and workspace size for a BF16 shard (as for pact_shard). */
+int64_t pact_digest_slots_bf16(const pact_shard_bf16* s);
+int64_t pact_workspace_bytes_bf16(const pact_shard_bf16* s);
+
 /* Measurement support, not part of the commit: streams the same bytes as a
  * commit (reads 4 fp32 arrays, writes 3 fp32 arrays and one 16-bit array,
  * 30 bytes per element) with no arithmetic beyond one add, so its rate is

@@ -96,6 +96,10 @@ def _load():
             f32p, f32p, f32p, f32p, u16p, u64, u64, ctypes.POINTER(_Hyper), u64,
         ]
         lib.oracle_commit_and_digest.restype = u64
+        lib.oracle_adamw_commit_bf16.argtypes = [u16p, u16p, u16p, u16p, u64, ctypes.POINTER(_Scalars)]
+        lib.oracle_adamw_commit_bf16.restype = None
+        lib.oracle_state_digest_bf16.argtypes = [u16p, u16p, u16p, u64, u64]
+        lib.oracle_state_digest_bf16.restype = u64
         lib.oracle_zero_grad.argtypes = [f32p, u64]
         lib.oracle_zero_grad.restype = None
         lib.oracle_count_outstanding.argtypes = [f32p, u64]
@@ -198,6 +202,33 @@ def commit_and_digest(p, g, m, v, bf16, h: Hyper, step: int, first_index: int) -
             ctypes.byref(_hyper(h)), step,
         )
     )
+
+
+def adamw_commit_bf16(p, g, m, v, h: Hyper, step: int) -> None:
+    """One commit in place on BF16 state (uint16 bit patterns)."""
+    n = p.size
+    for a, nm in ((p, "p"), (g, "g"), (m, "m"), (v, "v")):
+        _check(a, np.uint16, nm, n)
+    if step < 1:
+        raise ValueError("step counts from 1")
+    lib = _load()
+    sc = _Scalars()
+    lib.oracle_make_scalars(ctypes.byref(_hyper(h)), step, ctypes.byref(sc))
+    lib.oracle_adamw_commit_bf16(_ptr(p, ctypes.c_uint16), _ptr(g, ctypes.c_uint16), _ptr(m, ctypes.c_uint16),
+                                 _ptr(v, ctypes.c_uint16), n, ctypes.byref(sc))
+
+
+def state_digest_bf16(p, m, v, first_index: int) -> int:
+    n = p.size
+    for a, nm in ((p, "p"), (m, "m"), (v, "v")):
+        _check(a, np.uint16, nm, n)
+    return int(_load().oracle_state_digest_bf16(_ptr(p, ctypes.c_uint16), _ptr(m, ctypes.c_uint16),
+                                                _ptr(v, ctypes.c_uint16), n, first_index))
+
+
+def commit_and_digest_bf16(p, g, m, v, h: Hyper, step: int, first_index: int) -> int:
+    adamw_commit_bf16(p, g, m, v, h, step)
+    return state_digest_bf16(p, m, v, first_index)
 
 
 def zero_grad(g) -> None:

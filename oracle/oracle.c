@@ -103,37 +103,77 @@ void oracle_make_scalars(const oracle_hyper* h, uint64_t step, oracle_scalars* o
 /* weight, bias-corrected moments, eps added after the bias-corrected root.   */
 /* Each statement is one binary32 operation with one RNE rounding.            */
 /* ------------------------------------------------------------------------ */
+static void adamw_element(float* p, float grad, float* m, float* v, const oracle_scalars* sc) {
+    const float w = *p;
+    const float m_prev = *m;
+    const float v_prev = *v;
+
+    const float w_decayed = w * sc->decay;
+
+    const float m_keep = sc->beta1 * m_prev;
+    const float m_push = sc->omb1 * grad;
+    const float m_next = m_keep + m_push;
+
+    const float grad_sq = grad * grad;
+    const float v_keep = sc->beta2 * v_prev;
+    const float v_push = sc->omb2 * grad_sq;
+    const float v_next = v_keep + v_push;
+
+    const float root = sqrtf(v_next);
+    const float root_hat = root * sc->rs_bc2;
+    const float denom = root_hat + sc->eps;
+    const float ratio = m_next / denom;
+    const float delta = sc->step_size * ratio;
+    const float w_next = w_decayed - delta;
+
+    *p = w_next;
+    *m = m_next;
+    *v = v_next;
+}
+
 void oracle_adamw_commit(float* p, const float* g, float* m, float* v,
                          uint16_t* bf16, uint64_t n, const oracle_scalars* sc) {
     for (uint64_t i = 0; i < n; i++) {
-        const float w = p[i];
-        const float grad = g[i];
-        const float m_prev = m[i];
-        const float v_prev = v[i];
-
-        const float w_decayed = w * sc->decay;
-
-        const float m_keep = sc->beta1 * m_prev;
-        const float m_push = sc->omb1 * grad;
-        const float m_next = m_keep + m_push;
-
-        const float grad_sq = grad * grad;
-        const float v_keep = sc->beta2 * v_prev;
-        const float v_push = sc->omb2 * grad_sq;
-        const float v_next = v_keep + v_push;
-
-        const float root = sqrtf(v_next);
-        const float root_hat = root * sc->rs_bc2;
-        const float denom = root_hat + sc->eps;
-        const float ratio = m_next / denom;
-        const float delta = sc->step_size * ratio;
-        const float w_next = w_decayed - delta;
-
-        p[i] = w_next;
-        m[i] = m_next;
-        v[i] = v_next;
-        bf16[i] = oracle_bf16_rne(f32_bits(w_next));
+        adamw_element(&p[i], g[i], &m[i], &v[i], sc);
+        bf16[i] = oracle_bf16_rne(f32_bits(p[i]));
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* BF16 state, the paper's own precision for weights and moments (Sec. IV-A): */
+/* widen each word exactly, apply the same binary32 update, round p', m', v'  */
+/* back with the RNE rule above.                                               */
+/* ------------------------------------------------------------------------ */
+static float widen_bf16(uint16_t b) {
+    const uint32_t u = (uint32_t)b << 16;
+    float x;
+    memcpy(&x, &u, sizeof x);
+    return x;
+}
+
+void oracle_adamw_commit_bf16(uint16_t* p, const uint16_t* g, uint16_t* m, uint16_t* v,
+                              uint64_t n, const oracle_scalars* sc) {
+    for (uint64_t i = 0; i < n; i++) {
+        float w = widen_bf16(p[i]);
+        float mm = widen_bf16(m[i]);
+        float vv = widen_bf16(v[i]);
+        adamw_element(&w, widen_bf16(g[i]), &mm, &vv, sc);
+        p[i] = oracle_bf16_rne(f32_bits(w));
+        m[i] = oracle_bf16_rne(f32_bits(mm));
+        v[i] = oracle_bf16_rne(f32_bits(vv));
+    }
+}
+
+uint64_t oracle_state_digest_bf16(const uint16_t* p, const uint16_t* m, const uint16_t* v,
+                                  uint64_t n, uint64_t first_index) {
+    uint64_t sum = 0;
+    for (uint64_t i = 0; i < n; i++) {
+        const uint64_t index = first_index + i;
+        sum += oracle_splitmix64((uint64_t)p[i] ^ (index | (0ull << 56)));
+        sum += oracle_splitmix64((uint64_t)m[i] ^ (index | (1ull << 56)));
+        sum += oracle_splitmix64((uint64_t)v[i] ^ (index | (2ull << 56)));
+    }
+    return sum;
 }
 
 /* ------------------------------------------------------------------------ */

@@ -79,6 +79,17 @@ uint64_t oracle_state_digest(const float* p, const float* m, const float* v,
 /* Digest of the bf16 copy, tag 3, 16-bit words zero-extended. */
 uint64_t oracle_bf16_digest(const uint16_t* b, uint64_t n, uint64_t first_index);
 
+/* BF16 state (the paper's precision: BF16 weights and moments, Sec. IV-A).
+ * Each bf16 word is widened exactly to binary32 (bits << 16), the same
+ * binary32 update as oracle_adamw_commit is applied, and p', m', v' are
+ * rounded back to bf16 with oracle_bf16_rne. */
+void oracle_adamw_commit_bf16(uint16_t* p, const uint16_t* g, uint16_t* m, uint16_t* v,
+                              uint64_t n, const oracle_scalars* sc);
+
+/* Digest of BF16 state: the same sum with the 16-bit words, tags 0, 1, 2. */
+uint64_t oracle_state_digest_bf16(const uint16_t* p, const uint16_t* m, const uint16_t* v,
+                                  uint64_t n, uint64_t first_index);
+
 /* The committed boundary also has the flat gradients zeroed (Sec. I;
  * Sec. III-C, phase 2): every element of g becomes +0.0. */
 void oracle_zero_grad(float* g, uint64_t n);

@@ -23,8 +23,8 @@ from typing import Optional, Sequence, Tuple
 import torch
 
 __all__ = [
-    "Hyper", "Shard", "ShardArena", "PactError", "adamw_commit", "grad_guard", "shard_digest", "bf16_digest",
-    "stream_probe",
+    "Hyper", "Shard", "ShardBf16", "ShardArena", "PactError", "adamw_commit", "adamw_commit_bf16", "grad_guard",
+    "shard_digest", "shard_digest_bf16", "bf16_digest", "stream_probe",
     "digest_slots", "to_u64", "library_path",
 ]
 
@@ -63,6 +63,17 @@ class _CShard(ctypes.Structure):
     ]
 
 
+class _CShardBf16(ctypes.Structure):
+    _fields_ = [
+        ("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+        ("exp_avg_sq", ctypes.c_void_p),
+        ("numel", ctypes.c_uint64), ("global_offset", ctypes.c_uint64),
+        ("segs", ctypes.POINTER(_CSegment)), ("num_segs", ctypes.c_uint32), ("num_hypers", ctypes.c_uint32),
+        ("hypers", ctypes.POINTER(_CHyper)), ("digest_dev", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_uint64), ("stream", ctypes.c_void_p),
+    ]
+
+
 _LIB = None
 
 
@@ -82,6 +93,15 @@ def _lib():
         lib.pact_adamw_commit_ex.restype = ctypes.c_int
         lib.pact_grad_guard.argtypes = [P, ctypes.c_void_p]
         lib.pact_grad_guard.restype = ctypes.c_int
+        PB = ctypes.POINTER(_CShardBf16)
+        lib.pact_adamw_commit_bf16.argtypes = [PB, ctypes.c_uint64, ctypes.POINTER(_CHyper)]
+        lib.pact_adamw_commit_bf16.restype = ctypes.c_int
+        lib.pact_shard_digest_bf16.argtypes = [PB]
+        lib.pact_shard_digest_bf16.restype = ctypes.c_int
+        lib.pact_digest_slots_bf16.argtypes = [PB]
+        lib.pact_digest_slots_bf16.restype = ctypes.c_int64
+        lib.pact_workspace_bytes_bf16.argtypes = [PB]
+        lib.pact_workspace_bytes_bf16.restype = ctypes.c_int64
         lib.pact_shard_digest.argtypes = [P]
         lib.pact_shard_digest.restype = ctypes.c_int
         lib.pact_bf16_digest.argtypes = [P, ctypes.c_void_p]
@@ -196,6 +216,62 @@ class Shard:
         return s
 
 
+class ShardBf16:
+    """One rank's flat shard held in BF16 (the paper's precision for weights
+    and moments): param, grad, exp_avg, exp_avg_sq as int16/bfloat16 tensors
+    of bf16 bit patterns, and the digest slots.  Segments as for Shard."""
+
+    def __init__(self, param: torch.Tensor, grad: Optional[torch.Tensor], exp_avg: torch.Tensor,
+                 exp_avg_sq: torch.Tensor, global_offset: int = 0,
+                 segments: Optional[Sequence[Tuple[int, int, int]]] = None,
+                 hypers: Optional[Sequence[Hyper]] = None, use_workspace: bool = True):
+        n = param.numel()
+        b16 = (torch.bfloat16, torch.int16)
+        self.param = _dev_tensor(param, b16, "param", n)
+        self.grad = _dev_tensor(grad, b16, "grad", n)
+        self.exp_avg = _dev_tensor(exp_avg, b16, "exp_avg", n)
+        self.exp_avg_sq = _dev_tensor(exp_avg_sq, b16, "exp_avg_sq", n)
+        self.numel = n
+        self.global_offset = int(global_offset)
+        self.device = param.device
+        self.segments = None if segments is None else [tuple(int(x) for x in s) for s in segments]
+        self.hypers = None if hypers is None else list(hypers)
+        if self.segments is not None and not self.hypers:
+            raise ValueError("a segment table needs a hyper table")
+        self.slots = 1 if self.segments is None else len(self.segments) + 1
+        self.digest = torch.zeros(self.slots, dtype=torch.int64, device=self.device)
+        if self.segments is not None:
+            self._csegs = (_CSegment * len(self.segments))(*[_CSegment(o, l, h, 0) for o, l, h in self.segments])
+            self._chypers = (_CHyper * len(self.hypers))(*[h._c() for h in self.hypers])
+        else:
+            self._csegs = None
+            self._chypers = None
+        self.workspace = None
+        if use_workspace:
+            nbytes = int(_lib().pact_workspace_bytes_bf16(ctypes.byref(self._c())))
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+
+    def _c(self) -> _CShardBf16:
+        def ptr(t):
+            return None if t is None else t.data_ptr()
+
+        s = _CShardBf16()
+        s.param, s.grad, s.exp_avg, s.exp_avg_sq = (ptr(self.param), ptr(self.grad), ptr(self.exp_avg),
+                                                     ptr(self.exp_avg_sq))
+        s.numel, s.global_offset = self.numel, self.global_offset
+        if self._csegs is not None:
+            s.segs = ctypes.cast(self._csegs, ctypes.POINTER(_CSegment))
+            s.num_segs = len(self.segments)
+            s.hypers = ctypes.cast(self._chypers, ctypes.POINTER(_CHyper))
+            s.num_hypers = len(self.hypers)
+        s.digest_dev = self.digest.data_ptr()
+        ws = getattr(self, "workspace", None)
+        if ws is not None:
+            s.workspace, s.workspace_bytes = ws.data_ptr(), ws.numel()
+        s.stream = torch.cuda.current_stream(self.device).cuda_stream
+        return s
+
+
 class ShardArena:
     """Device memory for one shard's five arrays, each placed in its own
     region of HBM.
@@ -231,11 +307,13 @@ class ShardArena:
         # free gaps after each fp32 array: [start, end) in pool bytes
         self._gaps = [[k * self.spacing + f32, (k + 1) * self.spacing] for k in range(4)]
 
-    def take(self, nbytes: int, dtype=torch.uint8) -> torch.Tensor:
-        """A tensor carved from the space between the arrays (first fit,
-        256-byte aligned); raises if no gap is large enough."""
+    def take(self, nbytes: int, dtype=torch.uint8, region: Optional[int] = None) -> torch.Tensor:
+        """A tensor carved from the space between the arrays (first fit, or
+        the gap after array ``region`` in 0..3; 256-byte aligned); raises if
+        no gap is large enough."""
         esize = torch.empty((), dtype=dtype).element_size()
-        for gap in self._gaps:
+        gaps = self._gaps if region is None else [self._gaps[region]]
+        for gap in gaps:
             start = (gap[0] + 255) // 256 * 256
             if start + nbytes <= gap[1]:
                 gap[0] = start + nbytes
@@ -274,6 +352,26 @@ def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None, zero_gr
         rc = _lib().pact_adamw_commit_ex(ctypes.byref(shard._c()), int(step),
                                          ctypes.byref(ch) if ch is not None else None, flags)
     _call("pact_adamw_commit_ex", rc)
+    return shard.digest
+
+
+def adamw_commit_bf16(shard: ShardBf16, step: int, hyper: Optional[Hyper] = None) -> torch.Tensor:
+    """Commit one AdamW step on BF16 state (in place) and digest the result."""
+    if shard.segments is None and hyper is None:
+        hyper = Hyper()
+    ch = hyper._c() if hyper is not None else None
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_adamw_commit_bf16(ctypes.byref(shard._c()), int(step),
+                                           ctypes.byref(ch) if ch is not None else None)
+    _call("pact_adamw_commit_bf16", rc)
+    return shard.digest
+
+
+def shard_digest_bf16(shard: ShardBf16) -> torch.Tensor:
+    """Digest of the current BF16 (param, exp_avg, exp_avg_sq)."""
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_shard_digest_bf16(ctypes.byref(shard._c()))
+    _call("pact_shard_digest_bf16", rc)
     return shard.digest
 
 

@@ -1,7 +1,8 @@
 // kernels.hip -- gfx950 kernels of libpactshard.
 //
-// One tile kernel serves every mode (commit, commit that also zeroes the
-// gradient, state digest, bf16 digest, gradient guard).
+// One tile kernel serves every mode on binary32 state (commit, commit that
+// also zeroes the gradient, state digest, bf16 digest, gradient guard) and a
+// twin serves state held in BF16 (commit, state digest).
 // Work is cut into tiles of kTile elements that never straddle a segment, and
 // each workgroup takes exactly one tile (the hardware dispatcher then keeps
 // every CU full and balances the tail by itself; a persistent grid measured
@@ -278,9 +279,94 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
 // share is reduced across the workgroup and added to the segment's slot (or
 // the single total slot) with one 64-bit atomic.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// BF16 state: a tile is kTile / (kBlock * 8) rows of kBlock 16-byte vectors
+// (eight bf16 words each) per array; element 2j of a vector is the low half
+// of its word j.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float widen_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float widen_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
 template <Mode M>
-__global__ __launch_bounds__(kBlock) void tile_kernel(Arrays a, Batch bt) {
-    __shared__ uint64_t lds[kBlock / 64];
+__device__ __forceinline__ uint64_t do_scalar(const ArraysBf16& a, uint64_t e, const StepScalars& sc) {
+    const uint64_t idx = a.goff + e;
+    uint32_t p = a.p[e];
+    uint32_t m = a.m[e];
+    uint32_t v = a.v[e];
+    if constexpr (M == Mode::CommitBf16State) {
+        float pf = widen_lo(p), mf = widen_lo(m), vf = widen_lo(v);
+        adamw(pf, widen_lo(a.g[e]), mf, vf, sc);
+        p = to_bf16(pf);
+        m = to_bf16(mf);
+        v = to_bf16(vf);
+        a.p[e] = (uint16_t)p;
+        a.m[e] = (uint16_t)m;
+        a.v[e] = (uint16_t)v;
+    }
+    return hash_word(p, idx) + hash_word(m, idx | kTagM) + hash_word(v, idx | kTagV);
+}
+
+template <Mode M>
+__device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0, const StepScalars& sc) {
+    constexpr int kRows = kTile / (kBlock * 8);
+    constexpr uint32_t kRowBytes = kBlock * 16;
+    const uint32_t lane = threadIdx.x * 16;
+    const uint64_t lane_idx = a.goff + e0 + threadIdx.x * 8;
+    const auto rp = tile_rsrc(a.p + e0, kTile * 2);
+    const auto rm = tile_rsrc(a.m + e0, kTile * 2);
+    const auto rv = tile_rsrc(a.v + e0, kTile * 2);
+    u32x4 P[kRows], G[kRows], Mo[kRows], V[kRows];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+        P[r] = load16(rp, lane + r * kRowBytes);
+        Mo[r] = load16(rm, lane + r * kRowBytes);
+        V[r] = load16(rv, lane + r * kRowBytes);
+    }
+    if constexpr (M == Mode::CommitBf16State) {
+        const auto rg = tile_rsrc(a.g + e0, kTile * 2);
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            G[r] = load16(rg, lane + r * kRowBytes);
+        }
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float p0 = widen_lo(P[r][j]), p1 = widen_hi(P[r][j]);
+                float m0 = widen_lo(Mo[r][j]), m1 = widen_hi(Mo[r][j]);
+                float v0 = widen_lo(V[r][j]), v1 = widen_hi(V[r][j]);
+                adamw(p0, widen_lo(G[r][j]), m0, v0, sc);
+                adamw(p1, widen_hi(G[r][j]), m1, v1, sc);
+                P[r][j] = to_bf16(p0) | (to_bf16(p1) << 16);
+                Mo[r][j] = to_bf16(m0) | (to_bf16(m1) << 16);
+                V[r][j] = to_bf16(v0) | (to_bf16(v1) << 16);
+            }
+            store16(P[r], rp, lane + r * kRowBytes);
+            store16(Mo[r], rm, lane + r * kRowBytes);
+            store16(V[r], rv, lane + r * kRowBytes);
+        }
+    }
+    uint64_t acc = 0;
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint64_t i = lane_idx + (uint64_t)r * kBlock * 8 + 2 * j;
+            acc += hash_word(P[r][j] & 0xFFFFu, i) + hash_word(P[r][j] >> 16, i + 1) +
+                   hash_word(Mo[r][j] & 0xFFFFu, i | kTagM) + hash_word(Mo[r][j] >> 16, (i + 1) | kTagM) +
+                   hash_word(V[r][j] & 0xFFFFu, i | kTagV) + hash_word(V[r][j] >> 16, (i + 1) | kTagV);
+        }
+    }
+    return acc;
+}
+
+// ---------------------------------------------------------------------------
+// One workgroup per tile.  The tile's segment is found by binary search over
+// the batch's tile prefix (kernel arguments, scalar loads); the tile's digest
+// share is reduced across the workgroup and added with one 64-bit atomic.
+// ---------------------------------------------------------------------------
+template <Mode M, typename A>
+__device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t* lds) {
     const uint64_t tile = blockIdx.x;
     uint32_t lo = 0, hi = bt.nseg;  // largest lo with tile_begin[lo] <= tile
     while (hi - lo > 1) {
@@ -311,6 +397,18 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(Arrays a, Batch bt) {
         uint64_t* dst = a.lanes ? a.lanes + (r * kLanes + (blockIdx.x & (kLanes - 1))) * kLaneStride : a.digest + r;
         atomicAdd(reinterpret_cast<unsigned long long*>(dst), (unsigned long long)s);
     }
+}
+
+template <Mode M>
+__global__ __launch_bounds__(kBlock) void tile_kernel(Arrays a, Batch bt) {
+    __shared__ uint64_t lds[kBlock / 64];
+    tile_body<M>(a, bt, lds);
+}
+
+template <Mode M>
+__global__ __launch_bounds__(kBlock) void tile_kernel_bf16(ArraysBf16 a, Batch bt) {
+    __shared__ uint64_t lds[kBlock / 64];
+    tile_body<M>(a, bt, lds);
 }
 
 __global__ __launch_bounds__(kBlock) void clear_kernel(uint64_t* digest, uint64_t* lanes, uint32_t nres,
@@ -421,6 +519,20 @@ hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t gri
         case Mode::GradGuard:
             hipLaunchKernelGGL(tile_kernel<Mode::GradGuard>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_batch_bf16(Mode mode, const ArraysBf16& a, const Batch& b, uint32_t grid, hipStream_t stream) {
+    switch (mode) {
+        case Mode::CommitBf16State:
+            hipLaunchKernelGGL(tile_kernel_bf16<Mode::CommitBf16State>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            break;
+        case Mode::DigestBf16State:
+            hipLaunchKernelGGL(tile_kernel_bf16<Mode::DigestBf16State>, dim3(grid), dim3(kBlock), 0, stream, a, b);
+            break;
+        default:
+            return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -54,7 +54,26 @@ struct Arrays {
     uint64_t* lanes;    // workspace lanes, or null: atomics go to the result slots
 };
 
-enum class Mode : int { Commit = 0, StateDigest = 1, Bf16Digest = 2, CommitZeroGrad = 3, GradGuard = 4 };
+// The same arrays for a shard held in BF16 (no separate working copy).
+struct ArraysBf16 {
+    uint16_t* p;
+    const uint16_t* g;
+    uint16_t* m;
+    uint16_t* v;
+    uint64_t goff;
+    uint64_t* digest;
+    uint64_t* lanes;
+};
+
+enum class Mode : int {
+    Commit = 0,
+    StateDigest = 1,
+    Bf16Digest = 2,
+    CommitZeroGrad = 3,
+    GradGuard = 4,
+    CommitBf16State = 5,
+    DigestBf16State = 6,
+};
 
 // Enqueue the clearing of what the tile kernels accumulate into: the
 // nres * kLanes lane words when `lanes` is given, else the nslots digest slots.
@@ -63,6 +82,9 @@ hipError_t launch_clear(uint64_t* digest, uint64_t* lanes, uint32_t nres, uint32
 // Enqueue one batch in the given mode: one workgroup per tile, so `grid` is
 // the batch's tile count.
 hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t grid, hipStream_t stream);
+
+// Enqueue one batch of a BF16-state mode (CommitBf16State, DigestBf16State).
+hipError_t launch_batch_bf16(Mode mode, const ArraysBf16& a, const Batch& b, uint32_t grid, hipStream_t stream);
 
 // Enqueue the final sums: digest[r] = sum of r's lanes (when `lanes` is
 // given) for r < nres, and, with per-segment results, digest[nres] = their sum.

@@ -23,6 +23,64 @@ int fail_hip(hipError_t e) {
 }
 
 // ---------------------------------------------------------------------------
+// One view over either kind of shard: the five array slots are param, grad,
+// exp_avg, exp_avg_sq and the bf16 working copy; a BF16 shard has 2-byte
+// elements and no working copy.
+// ---------------------------------------------------------------------------
+enum Slot { kP = 0, kG = 1, kM = 2, kV = 3, kB = 4, kSlots = 5 };
+
+struct View {
+    const void* arr[kSlots];
+    uint32_t esize[kSlots];  // bytes per element (0: the shard has no such array)
+    uint64_t numel;
+    uint64_t goff;
+    const pact_segment* segs;
+    uint32_t num_segs;
+    uint32_t num_hypers;
+    const pact_hyper* hypers;
+    uint64_t* digest;
+    void* workspace;
+    uint64_t workspace_bytes;
+    void* stream;
+};
+
+template <typename S>
+View common_view(const S* s) {
+    View v;
+    v.arr[kP] = s->param;
+    v.arr[kG] = s->grad;
+    v.arr[kM] = s->exp_avg;
+    v.arr[kV] = s->exp_avg_sq;
+    v.numel = s->numel;
+    v.goff = s->global_offset;
+    v.segs = s->segs;
+    v.num_segs = s->num_segs;
+    v.num_hypers = s->num_hypers;
+    v.hypers = s->hypers;
+    v.digest = s->digest_dev;
+    v.workspace = s->workspace;
+    v.workspace_bytes = s->workspace_bytes;
+    v.stream = s->stream;
+    return v;
+}
+
+View view_of(const pact_shard* s) {
+    View v = common_view(s);
+    v.arr[kB] = s->param_bf16;
+    v.esize[kP] = v.esize[kG] = v.esize[kM] = v.esize[kV] = 4;
+    v.esize[kB] = 2;
+    return v;
+}
+
+View view_of(const pact_shard_bf16* s) {
+    View v = common_view(s);
+    v.arr[kB] = nullptr;
+    v.esize[kP] = v.esize[kG] = v.esize[kM] = v.esize[kV] = 2;
+    v.esize[kB] = 0;
+    return v;
+}
+
+// ---------------------------------------------------------------------------
 // validation
 // ---------------------------------------------------------------------------
 bool finite(float x) { return std::isfinite(x); }
@@ -50,38 +108,36 @@ bool overlaps(const std::vector<Span>& spans) {
 
 // Result slots that accumulate partial sums (one per segment, or one), and
 // the workspace bytes their lanes take.
-uint64_t result_slots(const pact_shard* s) { return s->segs ? (uint64_t)s->num_segs : 1; }
+uint64_t result_slots(const View& s) { return s.segs ? (uint64_t)s.num_segs : 1; }
 
-uint64_t workspace_need(const pact_shard* s) {
+uint64_t workspace_need(const View& s) {
     return result_slots(s) * pact::kLanes * pact::kLaneStride * sizeof(uint64_t);
 }
 
-// Which arrays a mode touches.
+// Which array slots a mode touches.
 struct Uses {
-    bool p, g, m, v, b;
+    bool slot[kSlots];
 };
 
 // Checks the shard for a mode; `out` is the digest destination.  Returns 0 or
 // a PACT_E* code.  Reads no device memory and makes no HIP call.
-int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t* nslots) {
-    if (s == nullptr || out == nullptr) return PACT_EINVAL;
-    const uint64_t n = s->numel;
-    if (n > 0) {
-        if ((use.p && !s->param) || (use.g && !s->grad) || (use.m && !s->exp_avg) ||
-            (use.v && !s->exp_avg_sq) || (use.b && !s->param_bf16)) {
-            return PACT_EINVAL;
-        }
+int validate(const View& s, const Uses& use, const uint64_t* out, uint64_t* nslots) {
+    if (out == nullptr) return PACT_EINVAL;
+    const uint64_t n = s.numel;
+    for (int k = 0; k < kSlots; ++k) {
+        if (use.slot[k] && s.esize[k] == 0) return PACT_EINVAL;  // this shard kind has no such array
+        if (use.slot[k] && n > 0 && s.arr[k] == nullptr) return PACT_EINVAL;
     }
-    if (s->global_offset >= kIndexLimit || n > kIndexLimit - s->global_offset) return PACT_ERANGE;
+    if (s.goff >= kIndexLimit || n > kIndexLimit - s.goff) return PACT_ERANGE;
     if (n > (UINT64_MAX / 4)) return PACT_ERANGE;
-    if ((n + pact::kTile - 1) / pact::kTile + (s->segs ? s->num_segs : 1) > (uint64_t)INT32_MAX) {
+    if ((n + pact::kTile - 1) / pact::kTile + (s.segs ? s.num_segs : 1) > (uint64_t)INT32_MAX) {
         return PACT_ERANGE;  // more tiles than one launch grid can hold
     }
-    if (s->segs != nullptr) {
-        if (s->num_segs == 0 || s->num_segs > kMaxSegments) return PACT_EINVAL;
+    if (s.segs != nullptr) {
+        if (s.num_segs == 0 || s.num_segs > kMaxSegments) return PACT_EINVAL;
         uint64_t prev_end = 0;
-        for (uint32_t k = 0; k < s->num_segs; ++k) {
-            const pact_segment& sg = s->segs[k];
+        for (uint32_t k = 0; k < s.num_segs; ++k) {
+            const pact_segment& sg = s.segs[k];
             if (sg.reserved != 0 || sg.offset < prev_end || sg.length > n || sg.offset > n - sg.length) {
                 return PACT_EINVAL;
             }
@@ -89,14 +145,13 @@ int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t
         }
     }
     if (!aligned(out, 8)) return PACT_EALIGN;
-    if ((use.p && !aligned(s->param, 4)) || (use.g && !aligned(s->grad, 4)) || (use.m && !aligned(s->exp_avg, 4)) ||
-        (use.v && !aligned(s->exp_avg_sq, 4)) || (use.b && !aligned(s->param_bf16, 2))) {
-        return PACT_EALIGN;
+    for (int k = 0; k < kSlots; ++k) {
+        if (use.slot[k] && !aligned(s.arr[k], s.esize[k])) return PACT_EALIGN;
     }
-    const uint64_t slots = s->segs ? (uint64_t)s->num_segs + 1 : 1;
-    if (s->workspace != nullptr) {
-        if (!aligned(s->workspace, 8)) return PACT_EALIGN;
-        if (s->workspace_bytes < workspace_need(s)) return PACT_EINVAL;
+    const uint64_t slots = s.segs ? (uint64_t)s.num_segs + 1 : 1;
+    if (s.workspace != nullptr) {
+        if (!aligned(s.workspace, 8)) return PACT_EALIGN;
+        if (s.workspace_bytes < workspace_need(s)) return PACT_EINVAL;
     }
     std::vector<Span> spans;
     auto add = [&](const void* ptr, uint64_t bytes) {
@@ -105,13 +160,11 @@ int validate(const pact_shard* s, const Uses& use, const uint64_t* out, uint64_t
             spans.push_back({lo, lo + bytes});
         }
     };
-    if (use.p) add(s->param, n * 4);
-    if (use.g) add(s->grad, n * 4);
-    if (use.m) add(s->exp_avg, n * 4);
-    if (use.v) add(s->exp_avg_sq, n * 4);
-    if (use.b) add(s->param_bf16, n * 2);
+    for (int k = 0; k < kSlots; ++k) {
+        if (use.slot[k]) add(s.arr[k], n * s.esize[k]);
+    }
     add(out, slots * 8);
-    if (s->workspace != nullptr) add(s->workspace, workspace_need(s));
+    if (s.workspace != nullptr) add(s.workspace, workspace_need(s));
     for (const Span& sp : spans) {
         if (sp.hi < sp.lo) return PACT_ERANGE;  // wraps the address space
     }
@@ -157,25 +210,64 @@ struct SegWork {
     pact::StepScalars sc;
 };
 
-int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots) {
-    hipStream_t stream = static_cast<hipStream_t>(s->stream);
-    uint64_t* lanes = static_cast<uint64_t*>(s->workspace);
+bool is_bf16_state(pact::Mode m) { return m == pact::Mode::CommitBf16State || m == pact::Mode::DigestBf16State; }
+
+// Whether a segment starting at element `first` can take the vector path:
+// 16-byte aligned in every array the mode moves as 16-byte vectors, 8-byte in
+// the bf16 working copy.
+bool vector_ok(pact::Mode mode, const View& s, uint64_t first) {
+    auto at = [&](int k, uintptr_t a) {
+        return aligned(static_cast<const char*>(s.arr[k]) + first * s.esize[k], a);
+    };
+    switch (mode) {
+        case pact::Mode::Bf16Digest:
+            return at(kB, 8);
+        case pact::Mode::GradGuard:
+            return at(kG, 16);
+        case pact::Mode::StateDigest:
+        case pact::Mode::DigestBf16State:
+            return at(kP, 16) && at(kM, 16) && at(kV, 16);
+        case pact::Mode::CommitBf16State:
+            return at(kP, 16) && at(kG, 16) && at(kM, 16) && at(kV, 16);
+        case pact::Mode::Commit:
+        case pact::Mode::CommitZeroGrad:
+            return at(kP, 16) && at(kG, 16) && at(kM, 16) && at(kV, 16) && at(kB, 8);
+    }
+    return false;
+}
+
+int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots) {
+    hipStream_t stream = static_cast<hipStream_t>(s.stream);
+    uint64_t* lanes = static_cast<uint64_t*>(s.workspace);
     const uint32_t nres = (uint32_t)result_slots(s);
     hipError_t e = pact::launch_clear(out, lanes, nres, (uint32_t)nslots, stream);
     if (e != hipSuccess) return fail_hip(e);
 
     pact::Arrays a;
-    a.p = s->param;
-    a.g = s->grad;
-    a.g_zero = const_cast<float*>(s->grad);  // written only by Mode::CommitZeroGrad
-    a.m = s->exp_avg;
-    a.v = s->exp_avg_sq;
-    a.b = s->param_bf16;
-    a.goff = s->global_offset;
-    a.digest = out;
-    a.lanes = lanes;
+    pact::ArraysBf16 ab;
+    std::memset(&a, 0, sizeof a);
+    std::memset(&ab, 0, sizeof ab);
+    if (is_bf16_state(mode)) {
+        ab.p = static_cast<uint16_t*>(const_cast<void*>(s.arr[kP]));
+        ab.g = static_cast<const uint16_t*>(s.arr[kG]);
+        ab.m = static_cast<uint16_t*>(const_cast<void*>(s.arr[kM]));
+        ab.v = static_cast<uint16_t*>(const_cast<void*>(s.arr[kV]));
+        ab.goff = s.goff;
+        ab.digest = out;
+        ab.lanes = lanes;
+    } else {
+        a.p = static_cast<float*>(const_cast<void*>(s.arr[kP]));
+        a.g = static_cast<const float*>(s.arr[kG]);
+        a.g_zero = const_cast<float*>(a.g);  // written only by Mode::CommitZeroGrad
+        a.m = static_cast<float*>(const_cast<void*>(s.arr[kM]));
+        a.v = static_cast<float*>(const_cast<void*>(s.arr[kV]));
+        a.b = static_cast<uint16_t*>(const_cast<void*>(s.arr[kB]));
+        a.goff = s.goff;
+        a.digest = out;
+        a.lanes = lanes;
+    }
 
-    const bool per_segment = s->segs != nullptr;
+    const bool per_segment = s.segs != nullptr;
     for (size_t first = 0; first < work.size(); first += pact::kSegsPerLaunch) {
         const size_t cnt = std::min<size_t>(pact::kSegsPerLaunch, work.size() - first);
         pact::Batch b;
@@ -191,22 +283,12 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
             b.elem_begin[k] = w.first;
             b.elem_count[k] = w.count;
             b.sc[k] = w.sc;
-            bool ok = true;
-            if (mode == pact::Mode::Bf16Digest) {
-                ok = aligned(a.b + w.first, 8);
-            } else if (mode == pact::Mode::GradGuard) {
-                ok = aligned(a.g + w.first, 16);
-            } else {
-                ok = aligned(a.p + w.first, 16) && aligned(a.m + w.first, 16) && aligned(a.v + w.first, 16);
-                if (mode == pact::Mode::Commit || mode == pact::Mode::CommitZeroGrad) {
-                    ok = ok && aligned(a.g + w.first, 16) && aligned(a.b + w.first, 8);
-                }
-            }
-            b.vec_ok[k] = ok ? 1u : 0u;
+            b.vec_ok[k] = vector_ok(mode, s, w.first) ? 1u : 0u;
         }
         b.tile_begin[cnt] = tiles;
         if (tiles == 0) continue;
-        e = pact::launch_batch(mode, a, b, (uint32_t)tiles, stream);
+        e = is_bf16_state(mode) ? pact::launch_batch_bf16(mode, ab, b, (uint32_t)tiles, stream)
+                                : pact::launch_batch(mode, a, b, (uint32_t)tiles, stream);
         if (e != hipSuccess) return fail_hip(e);
     }
     if (lanes != nullptr || per_segment) {
@@ -216,34 +298,56 @@ int run(pact::Mode mode, const pact_shard* s, const std::vector<SegWork>& work, 
     return PACT_OK;
 }
 
-std::vector<SegWork> segment_work(const pact_shard* s, const pact_hyper* single, uint64_t step, bool need_hyper,
+std::vector<SegWork> segment_work(const View& s, const pact_hyper* single, uint64_t step, bool need_hyper,
                                   int* err) {
     std::vector<SegWork> work;
     *err = PACT_OK;
-    if (s->segs == nullptr) {
-        SegWork w{0, s->numel, {}};
+    if (s.segs == nullptr) {
+        SegWork w{0, s.numel, {}};
         if (need_hyper) w.sc = step_scalars(*single, step);
-        if (s->numel > 0) work.push_back(w);
+        if (s.numel > 0) work.push_back(w);
         return work;
     }
-    if (need_hyper && s->hypers == nullptr) {
+    if (need_hyper && s.hypers == nullptr) {
         *err = PACT_EINVAL;
         return work;
     }
-    work.reserve(s->num_segs);
-    for (uint32_t k = 0; k < s->num_segs; ++k) {
-        const pact_segment& sg = s->segs[k];
+    work.reserve(s.num_segs);
+    for (uint32_t k = 0; k < s.num_segs; ++k) {
+        const pact_segment& sg = s.segs[k];
         SegWork w{sg.offset, sg.length, {}};
         if (need_hyper) {
-            if (sg.hyper_index >= s->num_hypers || !hyper_ok(s->hypers[sg.hyper_index])) {
+            if (sg.hyper_index >= s.num_hypers || !hyper_ok(s.hypers[sg.hyper_index])) {
                 *err = PACT_EINVAL;
                 return {};
             }
-            w.sc = step_scalars(s->hypers[sg.hyper_index], step);
+            w.sc = step_scalars(s.hypers[sg.hyper_index], step);
         }
         work.push_back(w);  // empty segments keep their slot (digest 0)
     }
     return work;
+}
+
+// A commit mode: check step and hyperparameters, validate, enqueue.
+int commit(pact::Mode mode, const View& s, uint64_t step, const pact_hyper* hyper, const Uses& use) {
+    if (step == 0) return PACT_EINVAL;
+    if (s.segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
+    uint64_t nslots = 0;
+    int rc = validate(s, use, s.digest, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(mode, s, work, s.digest, nslots);
+}
+
+// A mode that only reads the shard: validate, enqueue.
+int measure(pact::Mode mode, const View& s, const Uses& use, uint64_t* out) {
+    uint64_t nslots = 0;
+    int rc = validate(s, use, out, &nslots);
+    if (rc != PACT_OK) return rc;
+    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
+    if (rc != PACT_OK) return rc;
+    return run(mode, s, work, out, nslots);
 }
 
 }  // namespace
@@ -257,19 +361,24 @@ int64_t pact_digest_slots(const pact_shard* s) {
 
 int64_t pact_workspace_bytes(const pact_shard* s) {
     if (s == nullptr) return PACT_EINVAL;
-    return (int64_t)workspace_need(s);
+    return (int64_t)workspace_need(view_of(s));
+}
+
+int64_t pact_digest_slots_bf16(const pact_shard_bf16* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    return s->segs ? (int64_t)s->num_segs + 1 : 1;
+}
+
+int64_t pact_workspace_bytes_bf16(const pact_shard_bf16* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    return (int64_t)workspace_need(view_of(s));
 }
 
 int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags) {
-    if (s == nullptr || step == 0 || (flags & ~PACT_COMMIT_ZERO_GRAD) != 0) return PACT_EINVAL;
-    if (s->segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
-    uint64_t nslots = 0;
-    int rc = validate(s, Uses{true, true, true, true, true}, s->digest_dev, &nslots);
-    if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
-    if (rc != PACT_OK) return rc;
+    if (s == nullptr || (flags & ~PACT_COMMIT_ZERO_GRAD) != 0) return PACT_EINVAL;
+    const Uses use = {{true, true, true, true, true}};
     const pact::Mode mode = (flags & PACT_COMMIT_ZERO_GRAD) ? pact::Mode::CommitZeroGrad : pact::Mode::Commit;
-    return run(mode, s, work, s->digest_dev, nslots);
+    return commit(mode, view_of(s), step, hyper, use);
 }
 
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
@@ -278,32 +387,32 @@ int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hype
 
 int pact_grad_guard(const pact_shard* s, uint64_t* dev_out) {
     if (s == nullptr) return PACT_EINVAL;
-    uint64_t nslots = 0;
-    int rc = validate(s, Uses{false, true, false, false, false}, dev_out, &nslots);
-    if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
-    if (rc != PACT_OK) return rc;
-    return run(pact::Mode::GradGuard, s, work, dev_out, nslots);
+    const Uses use = {{false, true, false, false, false}};
+    return measure(pact::Mode::GradGuard, view_of(s), use, dev_out);
 }
 
 int pact_shard_digest(const pact_shard* s) {
     if (s == nullptr) return PACT_EINVAL;
-    uint64_t nslots = 0;
-    int rc = validate(s, Uses{true, false, true, true, false}, s->digest_dev, &nslots);
-    if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
-    if (rc != PACT_OK) return rc;
-    return run(pact::Mode::StateDigest, s, work, s->digest_dev, nslots);
+    const Uses use = {{true, false, true, true, false}};
+    return measure(pact::Mode::StateDigest, view_of(s), use, s->digest_dev);
 }
 
 int pact_bf16_digest(const pact_shard* s, uint64_t* dev_out) {
     if (s == nullptr) return PACT_EINVAL;
-    uint64_t nslots = 0;
-    int rc = validate(s, Uses{false, false, false, false, true}, dev_out, &nslots);
-    if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
-    if (rc != PACT_OK) return rc;
-    return run(pact::Mode::Bf16Digest, s, work, dev_out, nslots);
+    const Uses use = {{false, false, false, false, true}};
+    return measure(pact::Mode::Bf16Digest, view_of(s), use, dev_out);
+}
+
+int pact_adamw_commit_bf16(const pact_shard_bf16* s, uint64_t step, const pact_hyper* hyper) {
+    if (s == nullptr) return PACT_EINVAL;
+    const Uses use = {{true, true, true, true, false}};
+    return commit(pact::Mode::CommitBf16State, view_of(s), step, hyper, use);
+}
+
+int pact_shard_digest_bf16(const pact_shard_bf16* s) {
+    if (s == nullptr) return PACT_EINVAL;
+    const Uses use = {{true, false, true, true, false}};
+    return measure(pact::Mode::DigestBf16State, view_of(s), use, s->digest_dev);
 }
 
 int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
@@ -337,6 +446,6 @@ const char* pact_strerror(int code) {
 
 int pact_last_hip_error(void) { return g_last_hip_error; }
 
-int pact_version(void) { return 100; }
+int pact_version(void) { return 200; }
 
 }  // extern "C"

@@ -155,6 +155,24 @@ def test_commit_ex_and_guard_validation():
     assert lib.pact_grad_guard(ctypes.byref(fake_shard()), BASE + SPAN + 8) == pk.PACT_EOVERLAP
 
 
+def test_bf16_shard_validation():
+    from paper_2609_18178_amd import _CShardBf16
+
+    lib = pk._lib()
+    s = _CShardBf16()
+    s.param, s.grad, s.exp_avg, s.exp_avg_sq = (BASE + k * SPAN for k in range(4))
+    s.digest_dev = BASE + 5 * SPAN
+    s.numel = 1024
+    assert lib.pact_digest_slots_bf16(ctypes.byref(s)) == 1
+    assert lib.pact_workspace_bytes_bf16(ctypes.byref(s)) == 16 * 32 * 8
+    assert lib.pact_adamw_commit_bf16(ctypes.byref(s), 0, ctypes.byref(GOOD)) == pk.PACT_EINVAL
+    s.param = BASE + 1
+    assert lib.pact_adamw_commit_bf16(ctypes.byref(s), 1, ctypes.byref(GOOD)) == pk.PACT_EALIGN
+    s.param = BASE + SPAN + 2046  # last element overlaps grad's first
+    assert lib.pact_adamw_commit_bf16(ctypes.byref(s), 1, ctypes.byref(GOOD)) == pk.PACT_EOVERLAP
+    assert lib.pact_shard_digest_bf16(None) == pk.PACT_EINVAL
+
+
 def test_workspace_contract():
     lib = pk._lib()
     s = fake_shard()

@@ -449,3 +449,56 @@ def test_commit_zero_grad_and_guard(segmented):
     after = pk.to_u64(pk.grad_guard(sh))
     assert after == [0] * len(after)
     del torch
+
+
+def _bf16_arrays(w, start, count):
+    p, g, m, v = wl.arrays_host(w, start, count)
+    return [oracle.bf16_rne_bits(a.view(np.uint32)) for a in (p, g, m, v)]
+
+
+@pytest.mark.parametrize("n,shift", [(1, 0), (7, 3), (4096, 0), (4097, 0), (100003, 5), (1 << 20, 0)])
+def test_bf16_state_commit(n, shift):
+    """BF16 state (the paper's precision): p', m', v' and the digest bit for
+    bit, on ragged sizes and on views off the 16-byte grid."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    p, g, m, v = _bf16_arrays(w, 0, n)
+    full = [torch.zeros(n + 16, dtype=torch.int16, device="cuda") for _ in range(4)]
+    views = []
+    for t, a in zip(full, (p, g, m, v)):
+        t[shift:shift + n] = torch.from_numpy(a.view(np.int16)).cuda()
+        views.append(t[shift:shift + n])
+    sh = pk.ShardBf16(*views, global_offset=w.global_offset)
+    got = pk.to_u64(pk.adamw_commit_bf16(sh, 5, g_hyper(H)))[0]
+    want = oracle.commit_and_digest_bf16(p, g, m, v, o_hyper(H), 5, w.global_offset)
+    for name, t, ref in (("param", sh.param, p), ("exp_avg", sh.exp_avg, m), ("exp_avg_sq", sh.exp_avg_sq, v)):
+        assert_bitwise(name, host(t).view(np.uint16), ref)
+    assert got == want
+    assert pk.to_u64(pk.shard_digest_bf16(sh))[0] == want
+    for t in full:
+        h = host(t)
+        assert not h[:shift].any() and not h[shift + n:].any()
+
+
+def test_bf16_state_segments():
+    """BF16 state over the shrunken Mistral layout with per-segment hypers."""
+    import torch
+
+    pk = _pk()
+    w = wl.shrunken_mistral()
+    p, g, m, v = _bf16_arrays(w, 0, w.numel)
+    t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (p, g, m, v)]
+    sh = pk.ShardBf16(*t, global_offset=w.global_offset, segments=w.segments,
+                      hypers=[g_hyper(h) for h in w.hypers])
+    got = pk.to_u64(pk.adamw_commit_bf16(sh, 5))
+    per = []
+    for o, ln, hi in w.segments:
+        sl = slice(o, o + ln)
+        pp, gg, mm, vv = (a[sl].copy() for a in (p, g, m, v))
+        per.append(oracle.commit_and_digest_bf16(pp, gg, mm, vv, o_hyper(w.hypers[hi]), 5, w.global_offset + o))
+        p[sl], m[sl], v[sl] = pp, mm, vv
+    assert got == per + [sum(per) & M64]
+    for name, tt, ref in (("param", sh.param, p), ("exp_avg", sh.exp_avg, m), ("exp_avg_sq", sh.exp_avg_sq, v)):
+        assert_bitwise(name, host(tt).view(np.uint16), ref)

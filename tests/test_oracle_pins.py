@@ -430,3 +430,66 @@ def test_guard_counts_nonzero_bit_patterns():
     oracle.zero_grad(g)
     assert not g.view(np.uint32).any() and oracle.count_outstanding(g) == 0
     assert oracle.count_outstanding(np.zeros(0, np.float32)) == 0
+
+
+# ---------------------------------------------------------------------------
+# BF16 state (the paper's precision for weights and moments)
+# ---------------------------------------------------------------------------
+
+def _bf16_state(n, seed):
+    p, g, m, v = _fresh(n, seed, wl.NORMAL(1e-4), wl.ABS_NORMAL(1e-7))
+    return [oracle.bf16_rne_bits(a.view(np.uint32)) for a in (p, g, m, v)]
+
+
+def _widen(b):
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+def test_bf16_commit_is_the_rounded_binary32_commit():
+    """Pin against the pinned binary32 oracle and the pinned RNE rule: on
+    widened bf16 inputs, the bf16 commit's p', m', v' are exactly the RNE
+    roundings of the binary32 commit's results."""
+    n = 1 << 15
+    p, g, m, v = _bf16_state(n, 21)
+    P, G, Mm, V = (_widen(a).copy() for a in (p, g, m, v))
+    junk = np.empty(n, np.uint16)
+    oracle.adamw_commit(P, G, Mm, V, junk, H0, 7)
+    oracle.adamw_commit_bf16(p, g, m, v, H0, 7)
+    assert np.array_equal(p, oracle.bf16_rne_bits(P.view(np.uint32)))
+    assert np.array_equal(m, oracle.bf16_rne_bits(Mm.view(np.uint32)))
+    assert np.array_equal(v, oracle.bf16_rne_bits(V.view(np.uint32)))
+
+
+def test_bf16_first_step_closed_form():
+    """t = 1 from m = v = 0 on bf16 state: m' = RNE(f32((1-b1) g)), and p'
+    within half a bf16 ulp plus the binary32 bound of the real closed form."""
+    n = 1 << 14
+    p, g, _, _ = _bf16_state(n, 22)
+    m = np.zeros(n, np.uint16)
+    v = np.zeros(n, np.uint16)
+    p0, g64 = _widen(p).astype(np.float64), _widen(g).astype(np.float64)
+    oracle.adamw_commit_bf16(p, g, m, v, H0, 1)
+    omb1 = np.float32(1 - np.float32(0.9))
+    assert np.array_equal(m, oracle.bf16_rne_bits((omb1 * _widen(g)).view(np.uint32)))
+    lr, wd, eps = f32(H0.lr), f32(H0.weight_decay), f32(H0.eps)
+    u = lr * g64 / (np.abs(g64) + eps)
+    P = p0 * (1.0 - lr * wd) - u
+    got = _widen(p).astype(np.float64)
+    bf_ulp = np.spacing(np.abs(got).astype(np.float32)).astype(np.float64) * 65536.0
+    bound = 0.5 * bf_ulp + 0.5 * ulp(got) + 3 * ULP_EXP * np.abs(p0) + 12 * ULP_EXP * np.abs(u)
+    assert np.all(np.abs(got - P) <= bound)
+
+
+def test_bf16_digest_words_and_partitions():
+    """16-bit words are zero-extended; tags as for binary32 state; any
+    partition sums to the whole."""
+    z = np.zeros(1, np.uint16)
+    s = np.array([0x8000], np.uint16)
+    assert oracle.state_digest_bf16(s, z, z, 9) == (_f(0x8000 ^ 9) + _f(9 | 1 << 56) + _f(9 | 2 << 56)) & M64
+    rng = np.random.default_rng(23)
+    n = 5003
+    p, m, v = (rng.integers(0, 1 << 16, n, dtype=np.uint16) for _ in range(3))
+    whole = oracle.state_digest_bf16(p, m, v, 2 ** 40)
+    cuts = [0, 1, 2047, 4096, 5000, n]
+    parts = sum(oracle.state_digest_bf16(p[a:b], m[a:b], v[a:b], 2 ** 40 + a) for a, b in zip(cuts, cuts[1:]))
+    assert parts & M64 == whole
