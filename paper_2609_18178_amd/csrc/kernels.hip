@@ -41,10 +41,30 @@ constexpr uint64_t kTagM = 1ull << 56;
 constexpr uint64_t kTagV = 2ull << 56;
 constexpr uint64_t kTagB = 3ull << 56;
 
+// Low 64 bits of z * C for a constant C = CHI:CLO, in three VOP3
+// instructions: t = lo*CHI (v_mul_lo_u32); cross = hi*CLO + t, of which only
+// the low 32 bits are kept (v_mad_u64_u32); result = lo*CLO + cross << 32
+// (v_mad_u64_u32).  The compiler's own lowering takes four (two
+// v_mul_lo_u32, one v_mad_u64_u32, one v_add3_u32); on gfx950 every VOP3
+// instruction issues at about half the rate of a VOP2 one, so this is about
+// 13% faster on the hash.  VALU-only inline assembly (the carry-out operand
+// lands in a scalar register pair the result ignores).
+template <uint32_t CLO, uint32_t CHI>
+__device__ __forceinline__ uint64_t mul_const64(uint64_t z) {
+    const uint32_t lo = (uint32_t)z;
+    const uint32_t hi = (uint32_t)(z >> 32);
+    const uint32_t t = lo * CHI;
+    uint64_t cross, res, carry0, carry1;
+    asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cross), "=s"(carry0) : "v"(hi), "s"(CLO), "v"((uint64_t)t));
+    const uint64_t high = (uint64_t)(uint32_t)cross << 32;
+    asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(res), "=s"(carry1) : "v"(lo), "s"(CLO), "v"(high));
+    return res;
+}
+
 __device__ __forceinline__ uint64_t hash_word(uint32_t word, uint64_t tagged_index) {
     uint64_t z = ((uint64_t)word ^ tagged_index) + kGamma;
-    z = (z ^ (z >> 30)) * kMul1;
-    z = (z ^ (z >> 27)) * kMul2;
+    z = mul_const64<(uint32_t)kMul1, (uint32_t)(kMul1 >> 32)>(z ^ (z >> 30));
+    z = mul_const64<(uint32_t)kMul2, (uint32_t)(kMul2 >> 32)>(z ^ (z >> 27));
     return z ^ (z >> 31);
 }
 
@@ -75,12 +95,22 @@ __device__ __forceinline__ void adamw(float& p, float g, float& m, float& v, con
     v = v_new;
 }
 
-// binary32 -> bfloat16, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t to_bf16(float x) {
-    const uint32_t u = __float_as_uint(x);
-    const uint32_t rounded = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-    return ((u & 0x7FFFFFFFu) > 0x7F800000u) ? ((u >> 16) | 0x0040u) : rounded;
+// binary32 -> bfloat16, round to nearest even; NaN stays a quiet NaN with
+// its sign and top payload bits.  The rule, on the bits u of x:
+//   NaN:       (u >> 16) | 0x0040
+//   otherwise: (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+// gfx950's v_cvt_pk_bf16_f32 computes exactly this for every one of the 2^32
+// inputs (checked exhaustively on the device), two values per instruction,
+// so the kernels use it.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t to_bf16x2(float lo, float hi) {
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
+
+__device__ __forceinline__ uint32_t to_bf16(float x) { return to_bf16x2(x, 0.0f) & 0xFFFFu; }
 
 // ---------------------------------------------------------------------------
 // workgroup sum of a 64-bit value; result valid in thread 0
@@ -256,8 +286,8 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
                 store16(Mo[u], rm, lane32 + u * kRow32);
                 store16(V[u], rv, lane32 + u * kRow32);
                 u32x2 h;
-                h.x = to_bf16(p[0]) | (to_bf16(p[1]) << 16);
-                h.y = to_bf16(p[2]) | (to_bf16(p[3]) << 16);
+                h.x = to_bf16x2(p[0], p[1]);
+                h.y = to_bf16x2(p[2], p[3]);
                 store8(h, rb, lane16 + u * kRow16);
             }
         }
@@ -337,9 +367,9 @@ __device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0
                 float v0 = widen_lo(V[r][j]), v1 = widen_hi(V[r][j]);
                 adamw(p0, widen_lo(G[r][j]), m0, v0, sc);
                 adamw(p1, widen_hi(G[r][j]), m1, v1, sc);
-                P[r][j] = to_bf16(p0) | (to_bf16(p1) << 16);
-                Mo[r][j] = to_bf16(m0) | (to_bf16(m1) << 16);
-                V[r][j] = to_bf16(v0) | (to_bf16(v1) << 16);
+                P[r][j] = to_bf16x2(p0, p1);
+                Mo[r][j] = to_bf16x2(m0, m1);
+                V[r][j] = to_bf16x2(v0, v1);
             }
             store16(P[r], rp, lane + r * kRowBytes);
             store16(Mo[r], rm, lane + r * kRowBytes);
