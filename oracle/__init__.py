@@ -22,7 +22,8 @@ from typing import Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# PACT_ORACLE_LIB lets the mutation tests load a deliberately broken build.
+_LIB_PATH = os.environ.get("PACT_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 MASK64 = (1 << 64) - 1
 
