@@ -332,9 +332,16 @@ def main():
                 bstep[0] += 1
 
             kernels.append(("commit_bf16_state", bcommit, 14))
+        # what bounds each one on MI355X (rocprofv3 clock and VALU counters):
+        # HBM for the two that move 30+ B or a single array, VALU issue for the
+        # BF16-state commit (as much arithmetic as the binary32 commit on half
+        # the bytes), both for the digest (three hashes per 12 B)
+        bounds = {"commit_zero_grad": "hbm", "grad_guard": "hbm", "shard_digest": "hbm+valu",
+                  "commit_bf16_state": "valu"}
         for name, fn, bpe in kernels:
             ms = time_call(fn, reps)
-            extra[name] = {"ms": ms, "bytes_per_element": bpe, "gbps": bpe * n / (ms / 1e3) / 1e9,
+            extra[name] = {"ms": ms, "bound": bounds[name], "bytes_per_element": bpe,
+                           "gbps": bpe * n / (ms / 1e3) / 1e9,
                            "frac_of_peak": bpe * n / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS}
             print(f"[bench] {name}: {ms:.4f} ms, {extra[name]['gbps']:.1f} GB/s at {bpe} B/element",
                   file=sys.stderr, flush=True)

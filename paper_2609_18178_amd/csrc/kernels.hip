@@ -41,22 +41,29 @@ constexpr uint64_t kTagM = 1ull << 56;
 constexpr uint64_t kTagV = 2ull << 56;
 constexpr uint64_t kTagB = 3ull << 56;
 
-// Low 64 bits of z * C for a constant C = CHI:CLO, in three VOP3
-// instructions: t = lo*CHI (v_mul_lo_u32); cross = hi*CLO + t, of which only
-// the low 32 bits are kept (v_mad_u64_u32); result = lo*CLO + cross << 32
-// (v_mad_u64_u32).  The compiler's own lowering takes four (two
-// v_mul_lo_u32, one v_mad_u64_u32, one v_add3_u32); on gfx950 every VOP3
-// instruction issues at about half the rate of a VOP2 one, so this is about
-// 13% faster on the hash.  VALU-only inline assembly (the carry-out operand
-// lands in a scalar register pair the result ignores).
+// Low 64 bits of z * C for a constant C = CHI:CLO, as lo*CLO + (cross << 32)
+// with cross = hi*CLO + lo*CHI, of which only the low 32 bits matter:
+//   t     = lo * CHI              v_mul_lo_u32
+//   cross = hi * CLO + t          v_mad_u64_u32 (t zero-extended)
+//   high  = cross << 32           v_lshlrev_b64
+//   res   = lo * CLO + high       v_mad_u64_u32
+// The compiler's own lowering takes four multiply-class instructions, and
+// when left to build `high` itself it spends two register moves per multiply
+// assembling the (0, cross) pair; the single 64-bit shift replaces both.  The
+// hash is most of the VALU work of the commit, and under HBM traffic the
+// commit's VALU issue is what the reduced shader clock has to keep up with,
+// so each instruction saved here counts.  VALU-only inline assembly (the
+// carry-out operand lands in a scalar register pair the result ignores).
+// v_lshl_add_u64 would fold the shift into an add, but it only takes shift
+// amounts 0 to 4 on this chip.
 template <uint32_t CLO, uint32_t CHI>
 __device__ __forceinline__ uint64_t mul_const64(uint64_t z) {
     const uint32_t lo = (uint32_t)z;
     const uint32_t hi = (uint32_t)(z >> 32);
     const uint32_t t = lo * CHI;
-    uint64_t cross, res, carry0, carry1;
+    uint64_t cross, high, res, carry0, carry1;
     asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cross), "=s"(carry0) : "v"(hi), "s"(CLO), "v"((uint64_t)t));
-    const uint64_t high = (uint64_t)(uint32_t)cross << 32;
+    asm("v_lshlrev_b64 %0, 32, %1" : "=v"(high) : "v"(cross));
     asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(res), "=s"(carry1) : "v"(lo), "s"(CLO), "v"(high));
     return res;
 }
@@ -549,6 +556,8 @@ hipError_t launch_batch(Mode mode, const Arrays& a, const Batch& b, uint32_t gri
         case Mode::GradGuard:
             hipLaunchKernelGGL(tile_kernel<Mode::GradGuard>, dim3(grid), dim3(kBlock), 0, stream, a, b);
             break;
+        default:
+            return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
