@@ -52,6 +52,9 @@ def parse():
                          "(the library's recommended placement); packed: five separate allocations")
     ap.add_argument("--no-compare-layout", action="store_true",
                     help="skip timing the other layout as well")
+    ap.add_argument("--record-clock", metavar="CLOCK_CSV",
+                    help="write profiles/clock_<workload>.json (shader clock, VALU issue and VALU busy per kernel) "
+                         "from a rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_INSTS_VALU SQ_ACTIVE_INST_VALU run of bench.py")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) of a "
                          "bench run into profiles/traffic_<workload>.json and exit")
@@ -172,6 +175,67 @@ def _cpu_model() -> str:
     return "unknown"
 
 
+# rocprofv3 kernel names -> the names bench.py reports them under
+CLOCK_KERNELS = (("tile_kernel<(pact::Mode)0>", "commit", 30), ("probe_kernel(", "probe", 30),
+                 ("tile_kernel<(pact::Mode)3>", "commit_zero_grad", 34), ("tile_kernel<(pact::Mode)4>", "grad_guard", 4),
+                 ("tile_kernel<(pact::Mode)1>", "shard_digest", 12),
+                 ("tile_kernel_bf16<(pact::Mode)5>", "commit_bf16_state", 14))
+XCDS = 8      # GRBM_GUI_ACTIVE comes back summed over the eight XCDs
+NUM_CUS = 256
+
+
+def record_clock(workload: str, clock_csv: str) -> dict:
+    """Per kernel, from one counter run: duration (dispatch timestamps), shader
+    cycles (GRBM_GUI_ACTIVE per XCD), clock, VALU wave-instructions per element
+    and per CU per cycle, and rocprofv3's VALUBusy
+    (100 * SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE of one XCD)."""
+    import csv
+
+    import workloads as wl
+
+    n = wl.WORKLOADS[workload].numel
+    disp = {}
+    with open(clock_csv) as f:
+        for row in csv.DictReader(f):
+            hit = [(key, bpe) for pat, key, bpe in CLOCK_KERNELS if pat in row["Kernel_Name"]]
+            if not hit:
+                continue
+            d = disp.setdefault(int(row["Dispatch_Id"]), {"key": hit[0][0], "bpe": hit[0][1]})
+            d[row["Counter_Name"]] = float(row["Counter_Value"])
+            d["dur_s"] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) * 1e-9
+    kernels = {}
+    for d in disp.values():
+        kernels.setdefault(d["key"], []).append(d)
+    rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(), "kernels": {}}
+    for key, ds in kernels.items():
+        k = len(ds)
+        dur = sum(d["dur_s"] for d in ds) / k
+        cyc = sum(d["GRBM_GUI_ACTIVE"] for d in ds) / k / XCDS
+        valu = sum(d["SQ_INSTS_VALU"] for d in ds) / k
+        active = (sum(d["SQ_ACTIVE_INST_VALU"] for d in ds) / k) if "SQ_ACTIVE_INST_VALU" in ds[0] else None
+        rec["kernels"][key] = {
+            "dispatches": k, "us": dur * 1e6, "mcycles": cyc / 1e6, "clock_ghz": cyc / dur / 1e9,
+            "bytes_per_element": ds[0]["bpe"], "gbps": ds[0]["bpe"] * n / dur / 1e9,
+            "valu_instr_per_element": valu * 64 / n, "valu_issue_per_cu_cycle": valu / NUM_CUS / cyc,
+            "valu_busy_pct": None if active is None else 100.0 * active / NUM_CUS / cyc,
+        }
+    path = os.path.join(ROOT, "profiles", f"clock_{workload}.json")
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    return rec
+
+
+def stored_clock(workload: str, src_hash: str):
+    """The clock / VALU record of the current kernel source, if there is one."""
+    try:
+        with open(os.path.join(ROOT, "profiles", f"clock_{workload}.json")) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return rec if rec.get("kernel_source_hash") == src_hash else None
+
+
 def stored_traffic(workload: str, src_hash: str):
     """HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs of the
     current kernel source, if such a record exists."""
@@ -188,6 +252,9 @@ def stored_traffic(workload: str, src_hash: str):
 
 def main():
     args = parse()
+    if args.record_clock:
+        print(json.dumps(record_clock(args.workload, args.record_clock)))
+        return
     if args.record_traffic:
         print(json.dumps(record_traffic(args.workload, *args.record_traffic)))
         return
@@ -251,7 +318,7 @@ def main():
         wall = time.perf_counter() - wall0
         per_launch = [a.elapsed_time(b) for a, b in zip(ev_s, ev_e)]
         return {"ms_per_step": region_s.elapsed_time(region_e) / K, "avg_launch_ms": sum(per_launch) / K,
-                "min_launch_ms": min(per_launch), "wall_s": wall, "digest": pk.to_u64(sh.digest)[-1]}
+                "min_launch_ms": min(per_launch), "median_launch_ms": sorted(per_launch)[K // 2], "wall_s": wall, "digest": pk.to_u64(sh.digest)[-1]}
 
     def probe(tensors, bf16, K):
         p_s = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
@@ -373,6 +440,21 @@ def main():
     src_hash = kernel_source_hash()
     traffic_rec = stored_traffic(w.name, src_hash)
     traffic = None if traffic_rec is None else traffic_rec["bytes_per_launch"]
+    clock_rec = stored_clock(w.name, src_hash)
+    clock_k = {} if clock_rec is None else clock_rec["kernels"]
+
+    def valu_of(key):
+        c = clock_k.get(key)
+        if c is None:
+            return None
+        # busy_pct is rocprofv3's VALUBusy: four cycles per wave-instruction, so
+        # on gfx950 (some VALU instructions take fewer) it can pass 100
+        return {"busy_pct": c["valu_busy_pct"], "issue_per_cu_per_cycle": c["valu_issue_per_cu_cycle"],
+                "instr_per_element": c["valu_instr_per_element"], "clock_ghz": c["clock_ghz"],
+                "source": f"profiles/clock_{w.name}.json (rocprofv3 counters of this kernel source)"}
+
+    for name, entry in extra.items():
+        entry["valu"] = valu_of(name)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -408,6 +490,9 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": algo_bytes,
             "avg_launch_ms": avg_launch_ms,
+            "median_launch_ms": main_m["median_launch_ms"],
+            "min_launch_ms": main_m["min_launch_ms"],
+            "valu": valu_of("commit"),
             "timing": "hipEvents around each commit call on the launch stream; a call also runs the "
                       "one-workgroup kernels that clear and sum the digest lanes (a few microseconds)",
         },
