@@ -140,13 +140,15 @@ class Hyper:
         return _CHyper(self.lr, self.beta1, self.beta2, self.eps, self.weight_decay)
 
 
-def _dev_tensor(t: Optional[torch.Tensor], dtype, name: str, n: int):
+def _dev_tensor(t: Optional[torch.Tensor], dtype, name: str, n: int, device: Optional[torch.device] = None):
     if t is None:
         return None
     if not isinstance(t, torch.Tensor) or t.dtype not in dtype:
         raise TypeError(f"{name} must be a torch tensor of {dtype}")
     if t.device.type != "cuda":
         raise TypeError(f"{name} must live on a GPU (got {t.device}); there is no CPU path")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device} but param is on {device}: one shard lives on one GPU")
     if not t.is_contiguous() or t.numel() != n:
         raise ValueError(f"{name} must be contiguous with {n} elements")
     return t
@@ -169,10 +171,10 @@ class Shard:
         n = param.numel()
         f32 = (torch.float32,)
         self.param = _dev_tensor(param, f32, "param", n)
-        self.grad = _dev_tensor(grad, f32, "grad", n)
-        self.exp_avg = _dev_tensor(exp_avg, f32, "exp_avg", n)
-        self.exp_avg_sq = _dev_tensor(exp_avg_sq, f32, "exp_avg_sq", n)
-        self.param_bf16 = _dev_tensor(param_bf16, (torch.bfloat16, torch.int16), "param_bf16", n)
+        self.grad = _dev_tensor(grad, f32, "grad", n, param.device)
+        self.exp_avg = _dev_tensor(exp_avg, f32, "exp_avg", n, param.device)
+        self.exp_avg_sq = _dev_tensor(exp_avg_sq, f32, "exp_avg_sq", n, param.device)
+        self.param_bf16 = _dev_tensor(param_bf16, (torch.bfloat16, torch.int16), "param_bf16", n, param.device)
         self.numel = n
         self.global_offset = int(global_offset)
         self.device = param.device
@@ -228,9 +230,9 @@ class ShardBf16:
         n = param.numel()
         b16 = (torch.bfloat16, torch.int16)
         self.param = _dev_tensor(param, b16, "param", n)
-        self.grad = _dev_tensor(grad, b16, "grad", n)
-        self.exp_avg = _dev_tensor(exp_avg, b16, "exp_avg", n)
-        self.exp_avg_sq = _dev_tensor(exp_avg_sq, b16, "exp_avg_sq", n)
+        self.grad = _dev_tensor(grad, b16, "grad", n, param.device)
+        self.exp_avg = _dev_tensor(exp_avg, b16, "exp_avg", n, param.device)
+        self.exp_avg_sq = _dev_tensor(exp_avg_sq, b16, "exp_avg_sq", n, param.device)
         self.numel = n
         self.global_offset = int(global_offset)
         self.device = param.device
