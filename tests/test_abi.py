@@ -215,3 +215,27 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(pk, "library_path", "/nonexistent/libpactshard.so")
     with pytest.raises(RuntimeError, match="no fallback"):
         pk._lib()
+
+
+def test_header_is_c99_and_matches_the_binding(tmp_path):
+    """pactshard.h compiles as strict C99, and every struct the binding
+    mirrors with ctypes has the header's size and field offsets; the error
+    codes and flags agree too."""
+    import json
+    import subprocess
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    exe = tmp_path / "abi_layout"
+    subprocess.run(["gcc", "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-I", os.path.join(root, "include"),
+                    "-o", str(exe), os.path.join(root, "tests", "native", "abi_layout.c")], check=True)
+    c = json.loads(subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout)
+    mirrors = {"pact_hyper": pk._CHyper, "pact_segment": pk._CSegment, "pact_shard": pk._CShard,
+               "pact_shard_bf16": pk._CShardBf16}
+    for name, cls in mirrors.items():
+        assert ctypes.sizeof(cls) == c[name]["sizeof"], name
+        py_fields = {f[0]: getattr(cls, f[0]).offset for f in cls._fields_}
+        c_fields = c[name]["fields"]
+        # the binding names fields as the header does
+        assert py_fields == c_fields, (name, py_fields, c_fields)
+    for code, value in c["codes"].items():
+        assert getattr(pk, code) == value, code

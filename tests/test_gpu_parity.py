@@ -268,6 +268,86 @@ def test_special_values_lr_zero_keeps_every_pattern():
     del torch
 
 
+def _nan32(a):
+    u = np.asarray(a).view(np.uint32)
+    return (u & 0x7FFFFFFF) > 0x7F800000
+
+
+def _nan16(a):
+    u = np.asarray(a).view(np.uint16).astype(np.uint32)
+    return (u & 0x7FFF) > 0x7F80
+
+
+def _assert_same_or_both_nan(what, got, want, isnan):
+    """Bitwise where the oracle's result is a number; NaN where it is NaN (the
+    payload of a NaN made by an invalid operation is not part of the contract:
+    x86 makes 0xFFC00000, the GPU another pattern)."""
+    wn, gn = isnan(want), isnan(got)
+    assert np.array_equal(wn, gn), f"{what}: NaN at {np.flatnonzero(wn != gn)[:8]}"
+    keep = ~wn
+    assert_bitwise(what, np.asarray(got)[keep], np.asarray(want)[keep])
+
+
+@pytest.mark.parametrize("shift", [0, 1])
+def test_special_values_through_the_update(shift):
+    """Infinities, NaNs, overflowing and denormal gradients, infinite moments
+    and weights, planted in a realistic shard and sent through a full update
+    (lr > 0): every output bitwise where the oracle gives a number, NaN where
+    it gives NaN; the digest equals the oracle's digest of the GPU's own
+    outputs (it hashes whatever bits the update produced)."""
+    import torch
+
+    pk = _pk()
+    rng = np.random.default_rng(12)
+    n = 20011
+    p = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 3e-4).astype(np.float32) ** 2
+    f = lambda bits: np.array([bits], np.uint32).view(np.float32)[0]  # noqa: E731
+    specials_g = [np.inf, -np.inf, f(0x7FC00000), f(0x7FC12345), f(0xFFC00000), f(0x7F800001), 3e38, -3e38,
+                  1e30, -1e30, 1e20, f(0x00000001), f(0x80000001), -0.0, 0.0, np.finfo(np.float32).max]
+    specials_m = [np.inf, -np.inf, f(0x7FC00000), 3e38, -3e38, f(0x00000003)]
+    specials_v = [np.inf, f(0x7FC00000), 3e38, f(0x00000001), 0.0]
+    specials_p = [np.inf, -np.inf, f(0x7FC00000), np.finfo(np.float32).max, -np.finfo(np.float32).max,
+                  f(0x00000001), -0.0]
+    # plant each in the full tiles (vector path) and in the ragged tail
+    where = [3, 517, 4095, 4096, 9000, 12289, 16383, 20000, 20010]
+    for k, pos in enumerate(where):
+        for j, x in enumerate(specials_g):
+            g[(pos + 37 * j) % n] = x
+        for j, x in enumerate(specials_m):
+            m[(pos + 11 + 41 * j) % n] = x
+        for j, x in enumerate(specials_v):
+            v[(pos + 23 + 43 * j) % n] = x
+        for j, x in enumerate(specials_p):
+            p[(pos + 5 + 47 * j) % n] = x
+    # combinations: infinite gradient against an opposite infinite moment
+    g[100], m[100] = np.inf, -np.inf
+    g[101], v[101] = np.inf, np.inf
+    g[102], m[102], v[102] = f(0x7FC00000), np.inf, np.inf
+    base = 6_795_022_080
+    if shift:
+        p, g, m, v = (np.concatenate([np.zeros(shift, np.float32), a]) for a in (p, g, m, v))
+    tp, tg, tm, tv = (torch.from_numpy(a.copy()).cuda() for a in (p, g, m, v))
+    tb = torch.zeros(p.size, dtype=torch.int16, device="cuda")
+    sl = slice(shift, None)
+    sh = pk.Shard(tp[sl], tg[sl], tm[sl], tv[sl], tb[sl], global_offset=base)
+    hy = dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    d = pk.to_u64(pk.adamw_commit(sh, 7, g_hyper(hy)))[0]
+    pp, gg, mm, vv = (a[sl].copy() for a in (p, g, m, v))
+    b = np.zeros(n, np.uint16)
+    oracle.commit_and_digest(pp, gg, mm, vv, b, o_hyper(hy), 7, base)
+    got = [host(t[sl]) for t in (tp, tm, tv)]
+    for what, gval, want in zip(("param", "exp_avg", "exp_avg_sq"), got, (pp, mm, vv)):
+        _assert_same_or_both_nan(what, gval, want, _nan32)
+    _assert_same_or_both_nan("bf16", host(tb[sl]).view(np.uint16), b, _nan16)
+    assert _nan32(pp).sum() > 20 and np.isinf(pp).sum() > 10  # the plants did reach the outputs
+    assert d == oracle.state_digest(*got, base)
+    assert pk.to_u64(pk.shard_digest(sh))[0] == d
+    assert (host(tg[sl]).view(np.uint32) == g[sl].view(np.uint32)).all()  # the gradient is only read
+
+
 def test_denormal_state_is_kept():
     """Denormal moments and weights go through the update without flushing."""
     pk = _pk()
