@@ -348,6 +348,30 @@ def test_special_values_through_the_update(shift):
     assert (host(tg[sl]).view(np.uint32) == g[sl].view(np.uint32)).all()  # the gradient is only read
 
 
+def test_bias_correction_over_step_sequences():
+    """The library carries beta^t over from one call to the next; whatever
+    order the steps come in (forward, back to the start, far ahead, repeated)
+    every commit must equal the oracle's, which multiplies from 1 each time."""
+    pk = _pk()
+    rng = np.random.default_rng(21)
+    n = 4096 + 17
+    p0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    g0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    v0 = (np.abs(rng.standard_normal(n)) * 1e-7).astype(np.float32)
+    hypers = [dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1),
+              dict(lr=1e-4, beta1=0.95, beta2=0.9999, eps=1e-6, weight_decay=0.0)]
+    steps = [1, 2, 3, 1000, 1001, 5, 200000, 200001, 7, 2, 3000000, 3000001, 1]
+    for hy in hypers:
+        for t in steps:
+            sh = make_shard(p0, g0, m0, v0, 99)
+            d = pk.to_u64(pk.adamw_commit(sh, t, g_hyper(hy)))[0]
+            p, g, m, v = p0.copy(), g0.copy(), m0.copy(), v0.copy()
+            b = np.zeros(n, np.uint16)
+            assert d == oracle.commit_and_digest(p, g, m, v, b, o_hyper(hy), t, 99), (hy, t)
+            _compare_full(sh, p, m, v, b, f"t={t} ")
+
+
 def test_denormal_state_is_kept():
     """Denormal moments and weights go through the update without flushing."""
     pk = _pk()
