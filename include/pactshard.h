@@ -124,10 +124,13 @@ int64_t pact_digest_slots(const pact_shard* s);
  * instead of funnelling one 64-bit atomic per 4096-element tile into a single
  * address, which serializes on large shards.  The caller allocates it (8-byte
  * aligned, disjoint from every other buffer) and may reuse it for any later
- * call on the same stream; its contents on entry do not matter and on return
- * are unspecified.  workspace == NULL is valid: the call is then correct but
- * slower.  A non-NULL workspace with workspace_bytes below this figure is
- * PACT_EINVAL.  Negative error code if s is NULL. */
+ * call on the same stream.  Its contents on entry do not matter (the call
+ * clears the part it uses first, unless told with PACT_COMMIT_WORKSPACE_CLEAN
+ * that it is clear already), and every call that returns PACT_OK leaves that
+ * part zero again once the stream has run it.  workspace == NULL is valid:
+ * the call is then correct but slower.  A non-NULL workspace with
+ * workspace_bytes below this figure is PACT_EINVAL.  Negative error code if s
+ * is NULL. */
 int64_t pact_workspace_bytes(const pact_shard* s);
 
 /* The fused commit (Sec. III-A: the update after which W, M, V count as
@@ -137,7 +140,8 @@ int64_t pact_workspace_bytes(const pact_shard* s);
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper);
 
 /* Options of pact_adamw_commit_ex. */
-#define PACT_COMMIT_ZERO_GRAD 1u /* the same pass writes +0.0 into every committed grad element */
+#define PACT_COMMIT_ZERO_GRAD 1u       /* the same pass writes +0.0 into every committed grad element */
+#define PACT_COMMIT_WORKSPACE_CLEAN 2u /* the workspace is already clear: skip clearing it */
 
 /* The commit with options; flags = 0 is exactly pact_adamw_commit.
  * PACT_COMMIT_ZERO_GRAD: after reading g, the same pass writes +0.0 into
@@ -145,8 +149,12 @@ int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hype
  * so that one call leaves the shard at the boundary the paper admits for
  * in-memory recovery: update committed and flat gradients zeroed (Sec. I;
  * Sec. III-C, phase 2).  `grad` must then be writable device memory (the
- * const in pact_shard does not hold for this call).  Unknown flag bits are
- * PACT_EINVAL. */
+ * const in pact_shard does not hold for this call).
+ * PACT_COMMIT_WORKSPACE_CLEAN: the caller vouches that the workspace is clear
+ * (zero-filled before its first use, and touched since then only by calls on
+ * this stream that returned PACT_OK), so the call skips the launch that
+ * clears it; a workspace in any other state gives a wrong digest.  Without a
+ * workspace the flag has no effect.  Unknown flag bits are PACT_EINVAL. */
 int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags);
 
 /* Boundary guard for zero outstanding gradients (Sec. III-C, phase 2):

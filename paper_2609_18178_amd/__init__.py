@@ -191,11 +191,16 @@ class Shard:
         else:
             self._csegs = None
             self._chypers = None
-        # digest workspace: lets the partial sums spread over several addresses
+        # digest workspace: lets the partial sums spread over several addresses.
+        # Allocated zero-filled; every successful call leaves it so, which lets
+        # commits skip clearing it (workspace_clean stays true until a launch
+        # fails).
         self.workspace = None
+        self.workspace_clean = False
         if use_workspace:
             nbytes = int(_lib().pact_workspace_bytes(ctypes.byref(self._c())))
-            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=self.device)
+            self.workspace_clean = True
 
     def _c(self, digest_out: Optional[torch.Tensor] = None) -> _CShard:
         def ptr(t):
@@ -251,7 +256,7 @@ class ShardBf16:
         self.workspace = None
         if use_workspace:
             nbytes = int(_lib().pact_workspace_bytes_bf16(ctypes.byref(self._c())))
-            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=self.device)
 
     def _c(self) -> _CShardBf16:
         def ptr(t):
@@ -337,6 +342,17 @@ def digest_slots(shard: Shard) -> int:
 
 
 PACT_COMMIT_ZERO_GRAD = 1
+PACT_COMMIT_WORKSPACE_CLEAN = 2
+
+
+def _note_workspace(shard, rc: int) -> None:
+    """After a failed launch the workspace may hold partial sums: stop
+    vouching that it is clear (the next commit clears it, and the call after
+    that may skip the clearing again)."""
+    if rc == PACT_EHIP:
+        shard.workspace_clean = False
+    elif rc == PACT_OK and getattr(shard, "workspace", None) is not None:
+        shard.workspace_clean = True
 
 
 def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None, zero_grad: bool = False) -> torch.Tensor:
@@ -350,9 +366,12 @@ def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None, zero_gr
         hyper = Hyper()
     ch = hyper._c() if hyper is not None else None
     flags = PACT_COMMIT_ZERO_GRAD if zero_grad else 0
+    if shard.workspace is not None and shard.workspace_clean:
+        flags |= PACT_COMMIT_WORKSPACE_CLEAN
     with torch.cuda.device(shard.device):
         rc = _lib().pact_adamw_commit_ex(ctypes.byref(shard._c()), int(step),
                                          ctypes.byref(ch) if ch is not None else None, flags)
+    _note_workspace(shard, rc)
     _call("pact_adamw_commit_ex", rc)
     return shard.digest
 
@@ -383,6 +402,7 @@ def grad_guard(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tensor
         out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
     with torch.cuda.device(shard.device):
         rc = _lib().pact_grad_guard(ctypes.byref(shard._c()), out.data_ptr())
+    _note_workspace(shard, rc)
     _call("pact_grad_guard", rc)
     return out
 
@@ -391,6 +411,7 @@ def shard_digest(shard: Shard) -> torch.Tensor:
     """Digest of the shard's current (param, exp_avg, exp_avg_sq)."""
     with torch.cuda.device(shard.device):
         rc = _lib().pact_shard_digest(ctypes.byref(shard._c()))
+    _note_workspace(shard, rc)
     _call("pact_shard_digest", rc)
     return shard.digest
 
@@ -401,6 +422,7 @@ def bf16_digest(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tenso
         out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
     with torch.cuda.device(shard.device):
         rc = _lib().pact_bf16_digest(ctypes.byref(shard._c()), out.data_ptr())
+    _note_workspace(shard, rc)
     _call("pact_bf16_digest", rc)
     return out
 

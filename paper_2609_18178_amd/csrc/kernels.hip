@@ -463,8 +463,10 @@ __global__ __launch_bounds__(kBlock) void clear_kernel(uint64_t* digest, uint64_
 }
 
 // digest[r] = sum of r's lanes for r < nres (when lanes are used); with
-// per-segment results also digest[nres] = sum of digest[0..nres).
-__global__ __launch_bounds__(kBlock) void finish_kernel(uint64_t* digest, const uint64_t* lanes, uint32_t nres,
+// per-segment results also digest[nres] = sum of digest[0..nres).  Each lane
+// is set back to zero once read, so a call always leaves its workspace lanes
+// at zero and the next call may skip clearing them.
+__global__ __launch_bounds__(kBlock) void finish_kernel(uint64_t* digest, uint64_t* lanes, uint32_t nres,
                                                         uint32_t per_segment) {
     __shared__ uint64_t lds[kBlock / 64];
     uint64_t total = 0;
@@ -473,7 +475,9 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(uint64_t* digest, const 
         if (lanes) {
             x = 0;
             for (int l = 0; l < kLanes; ++l) {
-                x += lanes[((uint64_t)r * kLanes + l) * kLaneStride];
+                uint64_t* lane = lanes + ((uint64_t)r * kLanes + l) * kLaneStride;
+                x += *lane;
+                *lane = 0;
             }
             digest[r] = x;
         } else {

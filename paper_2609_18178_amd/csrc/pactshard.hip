@@ -283,12 +283,18 @@ bool vector_ok(pact::Mode mode, const View& s, uint64_t first) {
     return false;
 }
 
-int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots) {
+// workspace_clean: the caller vouches that the workspace lanes are zero (the
+// finish kernel leaves them so), and the clearing launch is skipped.
+int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots,
+        bool workspace_clean = false) {
     hipStream_t stream = static_cast<hipStream_t>(s.stream);
     uint64_t* lanes = static_cast<uint64_t*>(s.workspace);
     const uint32_t nres = (uint32_t)result_slots(s);
-    hipError_t e = pact::launch_clear(out, lanes, nres, (uint32_t)nslots, stream);
-    if (e != hipSuccess) return fail_hip(e);
+    hipError_t e = hipSuccess;
+    if (!(workspace_clean && lanes != nullptr)) {
+        e = pact::launch_clear(out, lanes, nres, (uint32_t)nslots, stream);
+        if (e != hipSuccess) return fail_hip(e);
+    }
 
     pact::Arrays a;
     pact::ArraysBf16 ab;
@@ -376,7 +382,8 @@ std::vector<SegWork> segment_work(const View& s, const pact_hyper* single, uint6
 }
 
 // A commit mode: check step and hyperparameters, validate, enqueue.
-int commit(pact::Mode mode, const View& s, uint64_t step, const pact_hyper* hyper, const Uses& use) {
+int commit(pact::Mode mode, const View& s, uint64_t step, const pact_hyper* hyper, const Uses& use,
+           bool workspace_clean = false) {
     if (step == 0) return PACT_EINVAL;
     if (s.segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
     uint64_t nslots = 0;
@@ -384,7 +391,7 @@ int commit(pact::Mode mode, const View& s, uint64_t step, const pact_hyper* hype
     if (rc != PACT_OK) return rc;
     std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
     if (rc != PACT_OK) return rc;
-    return run(mode, s, work, s.digest, nslots);
+    return run(mode, s, work, s.digest, nslots, workspace_clean);
 }
 
 // A mode that only reads the shard: validate, enqueue.
@@ -422,10 +429,10 @@ int64_t pact_workspace_bytes_bf16(const pact_shard_bf16* s) {
 }
 
 int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags) {
-    if (s == nullptr || (flags & ~PACT_COMMIT_ZERO_GRAD) != 0) return PACT_EINVAL;
+    if (s == nullptr || (flags & ~(PACT_COMMIT_ZERO_GRAD | PACT_COMMIT_WORKSPACE_CLEAN)) != 0) return PACT_EINVAL;
     const Uses use = {{true, true, true, true, true}};
     const pact::Mode mode = (flags & PACT_COMMIT_ZERO_GRAD) ? pact::Mode::CommitZeroGrad : pact::Mode::Commit;
-    return commit(mode, view_of(s), step, hyper, use);
+    return commit(mode, view_of(s), step, hyper, use, (flags & PACT_COMMIT_WORKSPACE_CLEAN) != 0);
 }
 
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {

@@ -144,7 +144,10 @@ def test_digest_slots():
 def test_commit_ex_and_guard_validation():
     lib = pk._lib()
     s = fake_shard()
-    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 1, ctypes.byref(GOOD), 2) == pk.PACT_EINVAL
+    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 1, ctypes.byref(GOOD), 4) == pk.PACT_EINVAL
+    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 1, ctypes.byref(GOOD), 0x80000000) == pk.PACT_EINVAL
+    # both known flags pass the flag check (and validation then stops at step 0)
+    assert lib.pact_adamw_commit_ex(ctypes.byref(s), 0, ctypes.byref(GOOD), 3) == pk.PACT_EINVAL
     assert lib.pact_adamw_commit_ex(ctypes.byref(s), 0, ctypes.byref(GOOD), 1) == pk.PACT_EINVAL
     assert lib.pact_adamw_commit_ex(ctypes.byref(fake_shard(grad=BASE)), 1, ctypes.byref(GOOD), 1) == \
         pk.PACT_EOVERLAP

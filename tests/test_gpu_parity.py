@@ -372,6 +372,69 @@ def test_bias_correction_over_step_sequences():
             _compare_full(sh, p, m, v, b, f"t={t} ")
 
 
+@pytest.mark.parametrize("segmented", [False, True])
+def test_workspace_is_left_clear_and_the_clean_flag_skips_clearing(segmented):
+    """Every call leaves the workspace lanes at zero, so commits through the
+    binding skip clearing them (PACT_COMMIT_WORKSPACE_CLEAN); mixed with the
+    digest and the guard, every result still equals the oracle's.  A dirty
+    workspace is cleared when the flag is not given, and gives a wrong digest
+    when it is (so the flag really skips the clearing)."""
+    import torch
+
+    pk = _pk()
+    rng = np.random.default_rng(31)
+    n = 3 * 4096 + 1000
+    p = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    v = (np.abs(rng.standard_normal(n)) * 1e-7).astype(np.float32)
+    segs = [(0, 5000, 0), (5000, 4000, 1), (9100, n - 9100, 0)] if segmented else None
+    hys = [dict(H), dict(H, lr=1e-4, weight_decay=0.0)]
+    sh = make_shard(p, g, m, v, 4242, segments=segs, hypers=hys if segmented else None)
+    assert sh.workspace is not None and sh.workspace_clean
+
+    b = np.zeros(n, np.uint16)
+
+    def expect_commit(step):
+        if segmented:
+            per, total = oracle.commit_segments(p, g, m, v, b, segs, [o_hyper(h) for h in hys], step, 4242)
+            return per + [total]
+        return [oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), step, 4242)]
+
+    def expect_digest():
+        if segmented:
+            per, total = oracle.segment_digests(p, m, v, segs, 4242)
+            return per + [total]
+        return [oracle.state_digest(p, m, v, 4242)]
+
+    lanes = 16 * (len(segs) if segmented else 1)  # 16 lanes per result slot, one word every 256 bytes
+
+    def workspace_zero():
+        words = sh.workspace.view(torch.int64)[::32][:lanes]
+        return int(torch.count_nonzero(words).item()) == 0
+
+    hy = None if segmented else g_hyper(H)
+    for step in (3, 4):
+        assert pk.to_u64(pk.adamw_commit(sh, step, hy)) == expect_commit(step)
+        assert workspace_zero()
+        assert pk.to_u64(pk.shard_digest(sh)) == expect_digest()
+        assert workspace_zero()
+        pk.grad_guard(sh)
+        assert workspace_zero()
+    # dirty workspace, flag not given: the call clears it first
+    sh.workspace.copy_(torch.randint(0, 256, sh.workspace.shape, dtype=torch.uint8, device=sh.workspace.device))
+    sh.workspace_clean = False
+    assert pk.to_u64(pk.adamw_commit(sh, 5, hy)) == expect_commit(5)
+    assert workspace_zero() and sh.workspace_clean
+    # dirty workspace with the flag: the clearing is skipped, the digest is off
+    sh.workspace.copy_(torch.randint(1, 256, sh.workspace.shape, dtype=torch.uint8, device=sh.workspace.device))
+    wrong = pk.to_u64(pk.adamw_commit(sh, 6, hy))
+    right = expect_commit(6)
+    assert wrong[0] != right[0]
+    _compare_full(sh, p, m, v, b)  # the state itself is committed correctly
+    assert workspace_zero()  # and the call still leaves the workspace clear
+
+
 def test_denormal_state_is_kept():
     """Denormal moments and weights go through the update without flushing."""
     pk = _pk()
