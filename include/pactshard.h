@@ -53,7 +53,11 @@
  * hipStream_t; NULL is the default stream) and returns; the digest slots
  * hold their value once the stream has reached that point.  Calls on one
  * stream are ordered; concurrent calls on different streams must not touch
- * the same buffers.
+ * the same buffers.  A call enqueues kernel launches only (no memset, no
+ * allocation, no host synchronisation), so it can be captured into a HIP
+ * graph; pointers, segment table, step and hyperparameters are taken at call
+ * time, so every replay of such a graph repeats the captured step on the
+ * same buffers.
  *
  * Errors.  0 on success, a negative PACT_E* code otherwise.  Argument errors
  * are found before anything is enqueued and leave every buffer untouched.

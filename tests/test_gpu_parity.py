@@ -435,6 +435,50 @@ def test_workspace_is_left_clear_and_the_clean_flag_skips_clearing(segmented):
     assert workspace_zero()  # and the call still leaves the workspace clear
 
 
+def test_commit_replays_from_a_hip_graph():
+    """A commit captured into a HIP graph (through torch's graph capture on the
+    current stream) replays as the same kernels: each replay equals one more
+    eager commit at the captured step, digests and state bit for bit, with
+    eager work and synchronisation between the replays."""
+    import torch
+
+    pk = _pk()
+    rng = np.random.default_rng(41)
+    n = 2 * 4096 + 333
+    p0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    g0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    v0 = (np.abs(rng.standard_normal(n)) * 1e-7).astype(np.float32)
+    hy = g_hyper(H)
+    eager = make_shard(p0, g0, m0, v0, 777)
+    want = []
+    for _ in range(3):
+        want.append(pk.to_u64(pk.adamw_commit(eager, 9, hy))[0])
+    graphed = make_shard(p0, g0, m0, v0, 777)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            pk.adamw_commit(graphed, 9, hy)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    # capture enqueues nothing: the state is untouched until the first replay
+    assert_bitwise("param before replay", host(graphed.param), p0)
+    for k in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        assert pk.to_u64(graphed.digest)[0] == want[k], k
+        _ = (torch.ones(1024, device="cuda") * 2).sum().item()  # unrelated eager work in between
+    for a, b in ((graphed.param, eager.param), (graphed.exp_avg, eager.exp_avg),
+                 (graphed.exp_avg_sq, eager.exp_avg_sq), (graphed.param_bf16, eager.param_bf16)):
+        assert torch.equal(a, b)
+    p, g, m, v = p0.copy(), g0.copy(), m0.copy(), v0.copy()
+    b = np.zeros(n, np.uint16)
+    for k in range(3):
+        assert oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), 9, 777) == want[k]
+
+
 def test_denormal_state_is_kept():
     """Denormal moments and weights go through the update without flushing."""
     pk = _pk()
