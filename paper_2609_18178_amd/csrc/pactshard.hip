@@ -500,6 +500,6 @@ const char* pact_strerror(int code) {
 
 int pact_last_hip_error(void) { return g_last_hip_error; }
 
-int pact_version(void) { return 200; }
+int pact_version(void) { return 300; }
 
 }  // extern "C"
