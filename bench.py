@@ -504,6 +504,9 @@ def main():
             "median_launch_ms": main_m["median_launch_ms"],
             "min_launch_ms": main_m["min_launch_ms"],
             "valu": valu_of("commit"),
+            # the same 30 B/element pattern with no arithmetic, in the same run:
+            # the practical ceiling of the access pattern (context, not the metric)
+            "frac_of_probe": (achieved / probe_res["gbps"]) if probe_res else None,
             "timing": "hipEvents around each commit call on the launch stream; a call also runs the "
                       "one-workgroup kernels that clear and sum the digest lanes (a few microseconds)",
         },
