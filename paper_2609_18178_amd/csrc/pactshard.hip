@@ -10,6 +10,16 @@
 
 #include "launch.h"
 
+// What the kernels and the batching below rely on.
+static_assert(pact::kBlock % 64 == 0 && pact::kBlock <= 1024, "whole waves of 64, one block");
+static_assert(pact::kVec == 4, "the binary32 vector path moves 16-byte vectors of four elements");
+static_assert(pact::kTile % (pact::kBlock * 8) == 0,
+              "a BF16-state tile is whole rows of 16-byte vectors of eight elements");
+static_assert((pact::kLanes & (pact::kLanes - 1)) == 0, "lane = workgroup & (kLanes - 1)");
+static_assert(pact::kLaneStride * sizeof(uint64_t) >= 128, "lanes sit in separate cache lines");
+static_assert((uint64_t)pact::kTile * 4 <= (1ull << 31), "a tile's byte offsets fit the 32-bit buffer offset");
+static_assert(pact::kSegsPerLaunch >= 1, "a launch takes at least one segment");
+
 namespace {
 
 thread_local int g_last_hip_error = 0;
