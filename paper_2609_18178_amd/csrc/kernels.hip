@@ -6,18 +6,22 @@
 // Work is cut into tiles of kTile elements that never straddle a segment, and
 // each workgroup takes exactly one tile (the hardware dispatcher then keeps
 // every CU full and balances the tail by itself; a persistent grid measured
-// slower on this pattern).  A full, aligned tile moves two 16-byte vectors
-// per array per thread with buffer_load/store_dwordx4 (bf16: dwordx2) marked
-// non-temporal; a ragged tail or a misaligned segment goes element by element.
+// slower on this pattern).  A full, aligned tile moves, per thread and per
+// binary32 array, four 16-byte vectors with buffer_load/store_dwordx4, and four
+// 8-byte ones into the bf16 working copy (dwordx2); on BF16 state, two 16-byte
+// vectors of eight elements per array.  All of it is marked non-temporal; a
+// ragged tail or a misaligned segment goes element by element.
 //
 // The digest is accumulated per thread in a 64-bit register (wrapping add),
 // reduced across the wave with shuffles and across the workgroup's four
 // waves through LDS, and added with one 64-bit atomic per workgroup into one
 // of kLanes workspace words of its result slot (256 bytes apart, so the
 // atomics of neighbouring workgroups do not queue on one address); a final
-// one-workgroup kernel sums the lanes.  Without a workspace the atomics go to
-// the result slot itself.  Wrapping addition is associative and commutative,
-// so the order in which workgroups arrive cannot change the result.
+// one-workgroup kernel sums the lanes and sets them back to zero, so a call
+// that is told its workspace is clear can skip clearing it.  Without a
+// workspace the atomics go to the result slot itself.  Wrapping addition is
+// associative and commutative, so the order in which workgroups arrive
+// cannot change the result.
 //
 // Arithmetic is the library contract in pactshard.h: one IEEE binary32
 // rounding per operation, no contraction or reassociation (the translation
@@ -310,12 +314,6 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
     }
 }
 
-// ---------------------------------------------------------------------------
-// One workgroup per tile.  The tile's segment is found by binary search over
-// the batch's tile prefix (kernel arguments, scalar loads); the tile's digest
-// share is reduced across the workgroup and added to the segment's slot (or
-// the single total slot) with one 64-bit atomic.
-// ---------------------------------------------------------------------------
 // ---------------------------------------------------------------------------
 // BF16 state: a tile is kTile / (kBlock * 8) rows of kBlock 16-byte vectors
 // (eight bf16 words each) per array; element 2j of a vector is the low half
