@@ -45,31 +45,31 @@ constexpr uint64_t kTagM = 1ull << 56;
 constexpr uint64_t kTagV = 2ull << 56;
 constexpr uint64_t kTagB = 3ull << 56;
 
-// Low 64 bits of z * C for a constant C = CHI:CLO, as lo*CLO + (cross << 32)
-// with cross = hi*CLO + lo*CHI, of which only the low 32 bits matter:
+// Low 64 bits of z * C for a constant C = CHI:CLO.  With z = hi:lo,
+//   z * C mod 2^64 = lo*CLO + ((hi*CLO + lo*CHI) << 32)
+// and only the low 32 bits of the cross term hi*CLO + lo*CHI matter:
 //   t     = lo * CHI              v_mul_lo_u32
-//   cross = hi * CLO + t          v_mad_u64_u32 (t zero-extended)
-//   high  = cross << 32           v_lshlrev_b64
-//   res   = lo * CLO + high       v_mad_u64_u32
-// The compiler's own lowering takes four multiply-class instructions, and
-// when left to build `high` itself it spends two register moves per multiply
-// assembling the (0, cross) pair; the single 64-bit shift replaces both.  The
-// hash is most of the VALU work of the commit, and under HBM traffic the
-// commit's VALU issue is what the reduced shader clock has to keep up with,
-// so each instruction saved here counts.  VALU-only inline assembly (the
-// carry-out operand lands in a scalar register pair the result ignores).
-// v_lshl_add_u64 would fold the shift into an add, but it only takes shift
-// amounts 0 to 4 on this chip.
+//   cross = hi * CLO + t          v_mad_u64_u32 (t zero-extended; low half used)
+//   prod  = lo * CLO              v_mad_u64_u32 (full 64-bit product)
+//   res   = prod + (cross << 32)  v_add_u32 on the high half
+// Three VOP3 instructions and one VOP2 add.  On gfx950 a VOP3 instruction
+// issues at about half the rate of a VOP2 one, and the hash is most of the
+// VALU work of every digesting kernel, so the cheaper add in place of a
+// 64-bit shift or a fourth multiply counts.  The compiler's own lowering
+// takes four multiply-class instructions plus register moves.  VALU-only
+// inline assembly (the carry-out operand lands in a scalar register pair the
+// result ignores).
 template <uint32_t CLO, uint32_t CHI>
 __device__ __forceinline__ uint64_t mul_const64(uint64_t z) {
     const uint32_t lo = (uint32_t)z;
     const uint32_t hi = (uint32_t)(z >> 32);
     const uint32_t t = lo * CHI;
-    uint64_t cross, high, res, carry0, carry1;
+    uint64_t cross, prod, carry0, carry1;
     asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cross), "=s"(carry0) : "v"(hi), "s"(CLO), "v"((uint64_t)t));
-    asm("v_lshlrev_b64 %0, 32, %1" : "=v"(high) : "v"(cross));
-    asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(res), "=s"(carry1) : "v"(lo), "s"(CLO), "v"(high));
-    return res;
+    asm("v_mad_u64_u32 %0, %1, %2, %3, 0" : "=v"(prod), "=s"(carry1) : "v"(lo), "s"(CLO));
+    uint32_t res_hi;
+    asm("v_add_u32_e32 %0, %1, %2" : "=v"(res_hi) : "v"((uint32_t)(prod >> 32)), "v"((uint32_t)cross));
+    return ((uint64_t)res_hi << 32) | (uint32_t)prod;
 }
 
 __device__ __forceinline__ uint64_t hash_word(uint32_t word, uint64_t tagged_index) {
