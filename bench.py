@@ -429,7 +429,7 @@ def main():
         other_layout = "packed" if args.layout == "spread" else "spread"
         del sh
         free, _ = torch.cuda.mem_get_info(dev)
-        need = 4 * n * 4 + 2 * n if other_layout == "packed" else 4 * (40 << 30) + 2 * n
+        need = 4 * n * 4 + 2 * n if other_layout == "packed" else 4 * pk.ARENA_SPACING + 2 * n
         if free > need + (2 << 30):
             o_arena, o_t, o_b = allocate(other_layout)
             fill(o_t, o_b)
@@ -487,7 +487,7 @@ def main():
         "data": "synthetic (seeded Philox4x32-10 inputs with the workload's shapes and distributions)",
         "config": dict(w.describe(), parallelism="one rank's shard, no collectives",
                        bytes_per_element=BYTES_PER_ELEM,
-                       layout=("spread: the five arrays in one ShardArena pool, 40 GiB apart"
+                       layout=(f"spread: the five arrays in one ShardArena pool, {pk.ARENA_SPACING >> 30} GiB apart"
                                if args.layout == "spread" else "packed: five separate torch allocations")),
         "hbm_gbps_nominal": algo_bytes / (ms_per_step / 1e3) / 1e9,
         "pct_of_peak_hbm": 100.0 * algo_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,

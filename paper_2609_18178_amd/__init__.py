@@ -279,27 +279,37 @@ class ShardBf16:
         return s
 
 
+# Default distance between the arrays of a ShardArena.
+ARENA_SPACING = 44 << 30
+
+
 class ShardArena:
     """Device memory for one shard's five arrays, each placed in its own
     region of HBM.
 
     On MI355X the commit's eight concurrent streams (reads of p, g, m, v;
     writes of p', m', v' and the bf16 copy) move about 5.6 TB/s when all five
-    arrays sit within a few gigabytes of each other, and about 6.45 TB/s when
-    they are spread over four or five regions some tens of gigabytes apart
-    (the same bytes, the same kernel; measured with the 30 B/element stream
-    probe and with the commit itself).  The arena takes one device pool and
-    puts array k at byte offset k * spacing, so the arrays land far apart in
-    physical memory; the space between them stays usable through take().
+    arrays sit within a few gigabytes of each other, and about 6.4-6.5 TB/s
+    when they are spread over four or five regions some tens of gigabytes
+    apart (the same bytes, the same kernel; measured with the 30 B/element
+    stream probe and with the commit itself).  The arena takes one device
+    pool and puts array k at byte offset k * spacing, so the arrays land far
+    apart in physical memory; the space between them stays usable through
+    take().
 
-    spacing: bytes between array starts (default 40 GiB, at least the
-    largest array).  The pool holds 4 * spacing + the bf16 array.
+    spacing: bytes between array starts (default ARENA_SPACING = 44 GiB, at
+    least the largest array).  The pool holds 4 * spacing + the bf16 array.
+    Among even spacings of 24-60 GiB, 44, 56, 58 and 60 GiB measured about 1%
+    faster than 36-42, 48 and 52 GiB on two boxes; 44 GiB is the smallest of
+    the fast ones.
     """
 
-    def __init__(self, numel: int, device=None, spacing: int = 40 << 30):
+    def __init__(self, numel: int, device=None, spacing: Optional[int] = None):
         device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
         if device.type != "cuda":
             raise TypeError("the arena lives on a GPU")
+        if spacing is None:
+            spacing = ARENA_SPACING
         align = 2 << 20
         f32 = (numel * 4 + align - 1) // align * align
         b16 = (numel * 2 + align - 1) // align * align
