@@ -78,7 +78,8 @@ extern "C" {
 #define PACT_EINVAL (-1)   /* null pointer, bad size, bad hyperparameter or segment table, step == 0 */
 #define PACT_EALIGN (-2)   /* misaligned pointer */
 #define PACT_EOVERLAP (-3) /* two buffers overlap */
-#define PACT_ERANGE (-4)   /* an index reaches 2^56 (the tag bits): global_offset + numel > 2^56 */
+#define PACT_ERANGE (-4)   /* an index reaches 2^56 (the tag bits): global_offset + numel > 2^56; or the
+                            * shard needs more than 2^24 - 1 tiles of 4096 elements (one launch grid) */
 #define PACT_EHIP (-5)     /* a HIP call failed; see pact_last_hip_error() */
 
 /* AdamW hyperparameters.  Valid: lr >= 0, 0 <= beta1 < 1, 0 <= beta2 < 1,

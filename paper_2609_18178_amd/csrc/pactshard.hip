@@ -140,20 +140,23 @@ int validate(const View& s, const Uses& use, const uint64_t* out, uint64_t* nslo
     }
     if (s.goff >= kIndexLimit || n > kIndexLimit - s.goff) return PACT_ERANGE;
     if (n > (UINT64_MAX / 4)) return PACT_ERANGE;
-    if ((n + pact::kTile - 1) / pact::kTile + (s.segs ? s.num_segs : 1) > (uint64_t)INT32_MAX) {
-        return PACT_ERANGE;  // more tiles than one launch grid can hold
-    }
+    uint64_t tiles = (n + pact::kTile - 1) / pact::kTile;
     if (s.segs != nullptr) {
         if (s.num_segs == 0 || s.num_segs > kMaxSegments) return PACT_EINVAL;
         uint64_t prev_end = 0;
+        tiles = 0;
         for (uint32_t k = 0; k < s.num_segs; ++k) {
             const pact_segment& sg = s.segs[k];
             if (sg.reserved != 0 || sg.offset < prev_end || sg.length > n || sg.offset > n - sg.length) {
                 return PACT_EINVAL;
             }
             prev_end = sg.offset + sg.length;
+            tiles += (sg.length + pact::kTile - 1) / pact::kTile;  // tiles never straddle segments
         }
     }
+    // A dispatch counts its work-items in 32 bits, so one launch holds at most
+    // UINT32_MAX / kBlock tiles; the total bounds every launch's share.
+    if (tiles > (uint64_t)(UINT32_MAX / pact::kBlock)) return PACT_ERANGE;
     if (!aligned(out, 8)) return PACT_EALIGN;
     for (int k = 0; k < kSlots; ++k) {
         if (use.slot[k] && !aligned(s.arr[k], s.esize[k])) return PACT_EALIGN;

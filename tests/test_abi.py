@@ -99,6 +99,11 @@ def test_range_errors():
     assert commit(fake_shard(n=16, global_offset=(1 << 56) - 15)) == pk.PACT_ERANGE
     assert commit(fake_shard(n=0, global_offset=1 << 56)) == pk.PACT_ERANGE
     assert commit(fake_shard(n=1 << 62)) == pk.PACT_ERANGE
+    # one launch grid holds at most (2^32 - 1) // 256 workgroups of one 4096-element tile each
+    max_tiles = ((1 << 32) - 1) // 256
+    assert commit(fake_shard(n=(max_tiles + 1) * 4096)) == pk.PACT_ERANGE
+    # a grid that just fits passes this check and fails later, on the overlapping fake arrays
+    assert commit(fake_shard(n=max_tiles * 4096)) == pk.PACT_EOVERLAP
 
 
 def _with_segs(segs, hypers=(GOOD,), n=1024):
