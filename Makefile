@@ -25,7 +25,12 @@ ORACLE_FLAGS := -O2 -std=c11 -ffp-contract=off -fno-fast-math -fno-math-errno \
                 -fexcess-precision=standard -fPIC -shared -Wall -Wextra
 GEN_FLAGS    := -O3 -std=c11 -fopenmp -fPIC -shared -Wall -Wextra
 
-all: oracle/liboracle.so workloads/libgen.so $(if $(LIB_SRCS),$(LIB),)
+# A plain C caller of the library (test infrastructure: it links the oracle
+# to check what the library computes); finds the in-tree libraries by rpath.
+C_CALLER := tests/native/c_caller
+ROCM     ?= /opt/rocm
+
+all: oracle/liboracle.so workloads/libgen.so $(if $(LIB_SRCS),$(LIB) $(C_CALLER),)
 
 oracle/liboracle.so: oracle/oracle.c oracle/oracle.h
 	$(CC) $(ORACLE_FLAGS) -o $@ oracle/oracle.c -lm
@@ -36,6 +41,12 @@ workloads/libgen.so: workloads/gen.c
 $(LIB): $(LIB_SRCS) $(LIB_HDRS)
 	$(HIPCC) $(HIPFLAGS) -o $@ $(LIB_SRCS)
 
+$(C_CALLER): tests/native/c_caller.c include/pactshard.h oracle/oracle.h $(LIB) oracle/liboracle.so workloads/libgen.so
+	$(CC) -std=c99 -O2 -Wall -Wextra -D__HIP_PLATFORM_AMD__ -Iinclude -Ioracle -I$(ROCM)/include -o $@ $< \
+	    -L$(PKG) -lpactshard -Loracle -loracle -Lworkloads -lgen -L$(ROCM)/lib -lamdhip64 \
+	    -Wl,-rpath,'$$ORIGIN/../../$(PKG)' -Wl,-rpath,'$$ORIGIN/../../oracle' -Wl,-rpath,'$$ORIGIN/../../workloads' \
+	    -Wl,-rpath,$(ROCM)/lib
+
 # gfx950 assembly of the kernels, for inspection and the hazard test
 isa: _build/kernels-gfx950.s
 _build/kernels-gfx950.s: $(PKG)/csrc/kernels.hip $(LIB_HDRS)
@@ -43,7 +54,7 @@ _build/kernels-gfx950.s: $(PKG)/csrc/kernels.hip $(LIB_HDRS)
 	$(HIPCC) $(filter-out -shared -fPIC,$(HIPFLAGS)) --cuda-device-only -S -o $@ $(PKG)/csrc/kernels.hip
 
 clean:
-	rm -f $(LIB) oracle/liboracle.so workloads/libgen.so
+	rm -f $(LIB) oracle/liboracle.so workloads/libgen.so $(C_CALLER)
 	rm -rf _build
 
 .PHONY: all clean isa

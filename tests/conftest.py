@@ -12,6 +12,7 @@ _LIBS = (
     os.path.join(ROOT, "oracle", "liboracle.so"),
     os.path.join(ROOT, "workloads", "libgen.so"),
     os.path.join(ROOT, "paper_2609_18178_amd", "libpactshard.so"),
+    os.path.join(ROOT, "tests", "native", "c_caller"),
 )
 
 
