@@ -41,9 +41,7 @@ namespace {
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kMul1 = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kMul2 = 0x94D049BB133111EBull;
-constexpr uint64_t kTagM = 1ull << 56;
-constexpr uint64_t kTagV = 2ull << 56;
-constexpr uint64_t kTagB = 3ull << 56;
+constexpr uint32_t kTagP = 0, kTagM = 1, kTagV = 2, kTagB = 3;  // array tags (bits 56..63 of the index)
 
 // Low 64 bits of z * C for a constant C = CHI:CLO.  With z = hi:lo,
 //   z * C mod 2^64 = lo*CLO + ((hi*CLO + lo*CHI) << 32)
@@ -72,11 +70,71 @@ __device__ __forceinline__ uint64_t mul_const64(uint64_t z) {
     return ((uint64_t)res_hi << 32) | (uint32_t)prod;
 }
 
-__device__ __forceinline__ uint64_t hash_word(uint32_t word, uint64_t tagged_index) {
-    uint64_t z = ((uint64_t)word ^ tagged_index) + kGamma;
+// The mixing function applied after the generator's first addition.
+__device__ __forceinline__ uint64_t splitmix_mix(uint64_t z) {
     z = mul_const64<(uint32_t)kMul1, (uint32_t)(kMul1 >> 32)>(z ^ (z >> 30));
     z = mul_const64<(uint32_t)kMul2, (uint32_t)(kMul2 >> 32)>(z ^ (z >> 27));
     return z ^ (z >> 31);
+}
+
+// splitmix64 of  word ^ (index | Tag << 56)  for a word of array Tag at flat
+// index `index`.  Indices stay below 2^56 (the host rejects larger ones) and
+// a word has 32 bits, so the tag bits meet only zeros on both sides:
+//   word ^ (index | Tag << 56) = (word ^ index) + (Tag << 56)
+// and the tag folds into the constant the generator adds first,
+//   z = (word ^ index) + (gamma + (Tag << 56))  mod 2^64.
+template <uint32_t Tag>
+__device__ __forceinline__ uint64_t hash_word(uint32_t word, uint64_t index) {
+    static_assert(Tag < 4, "array tags 0..3");
+    constexpr uint64_t kAdd = kGamma + ((uint64_t)Tag << 56);
+    return splitmix_mix(((uint64_t)word ^ index) + kAdd);
+}
+
+// The indices of the digest words of one vector tile, as seen by one lane:
+// word `off` of the lane sits at flat index first + off.
+//
+// IndexAny: plain 64-bit indices, valid for every tile.
+struct IndexAny {
+    uint64_t first;  // index of the lane's first word
+    __device__ __forceinline__ IndexAny(uint64_t tile_first, uint32_t lane_off) : first(tile_first + lane_off) {}
+    template <uint32_t Tag>
+    __device__ __forceinline__ uint64_t hash(uint32_t word, uint32_t off) const {
+        return hash_word<Tag>(word, first + off);
+    }
+};
+
+// IndexHi32: for a tile whose indices all share their upper 32 bits `hi`
+// (every tile but one that crosses a multiple of 2^32).  With index = hi:lo
+// the word only meets the low half, so
+//   (word ^ index) + gamma_k = zext(word ^ lo) + ((hi << 32) + gamma_k)
+// where gamma_k = gamma + (k << 56) is the tagged constant above.  The right
+// term is one wave-uniform 64-bit value per tag, kept in scalar registers,
+// and the sum is one v_mad_u64_u32 (word ^ lo) * 1 + G_k: no 64-bit index
+// arithmetic and no register pair to assemble for each word.
+struct IndexHi32 {
+    uint32_t lo;   // low half of the lane's first index
+    uint64_t g[4]; // (hi << 32) + gamma + (tag << 56) for tags 0..3
+    __device__ __forceinline__ IndexHi32(uint64_t tile_first, uint32_t lane_off)
+        : lo((uint32_t)tile_first + lane_off) {
+        const uint64_t high = tile_first & 0xFFFFFFFF00000000ull;
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k) {
+            g[k] = high + kGamma + ((uint64_t)k << 56);
+        }
+    }
+    template <uint32_t Tag>
+    __device__ __forceinline__ uint64_t hash(uint32_t word, uint32_t off) const {
+        static_assert(Tag < 4, "array tags 0..3");
+        const uint32_t x = word ^ (lo + off);
+        uint64_t z, carry;
+        asm("v_mad_u64_u32 %0, %1, %2, 1, %3" : "=v"(z), "=s"(carry) : "v"(x), "s"(g[Tag]));
+        return splitmix_mix(z);
+    }
+};
+
+// Whether the `count` indices from `first` on share their upper 32 bits.
+__device__ __forceinline__ bool same_high_half(uint64_t first, uint64_t count) {
+    return (first >> 32) == ((first + count - 1) >> 32);
 }
 
 // ---------------------------------------------------------------------------
@@ -191,7 +249,7 @@ template <Mode M>
 __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const StepScalars& sc) {
     const uint64_t idx = a.goff + e;
     if constexpr (M == Mode::Bf16Digest) {
-        return hash_word(a.b[e], idx | kTagB);
+        return hash_word<kTagB>(a.b[e], idx);
     } else if constexpr (M == Mode::GradGuard) {
         return __float_as_uint(a.g[e]) != 0u ? 1u : 0u;
     } else {
@@ -208,8 +266,8 @@ __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const
                 a.g_zero[e] = 0.0f;
             }
         }
-        return hash_word(__float_as_uint(p), idx) + hash_word(__float_as_uint(m), idx | kTagM) +
-               hash_word(__float_as_uint(v), idx | kTagV);
+        return hash_word<kTagP>(__float_as_uint(p), idx) + hash_word<kTagM>(__float_as_uint(m), idx) +
+               hash_word<kTagV>(__float_as_uint(v), idx);
     }
 }
 
@@ -218,13 +276,13 @@ __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const
 // the bf16 array): kUnroll rows of kBlock 16-byte vectors per array.  Row u,
 // lane t holds elements e0 + u*kBlock*4 + 4t .. +3.
 // ---------------------------------------------------------------------------
-template <Mode M>
+template <Mode M, typename Ix>
 __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, const StepScalars& sc) {
     constexpr uint32_t kRow32 = kBlock * kVec * 4;  // bytes of one fp32 row
     constexpr uint32_t kRow16 = kBlock * kVec * 2;  // bytes of one bf16 row
     const uint32_t lane32 = threadIdx.x * kVec * 4;
     const uint32_t lane16 = threadIdx.x * kVec * 2;
-    const uint64_t lane_idx = a.goff + e0 + threadIdx.x * kVec;
+    const Ix ix(a.goff + e0, threadIdx.x * kVec);  // word k of this lane: index + k
     uint64_t acc = 0;
     if constexpr (M == Mode::GradGuard) {
         const auto rg = tile_rsrc(a.g + e0, kTile * 4);
@@ -250,9 +308,9 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const uint64_t i = lane_idx + (uint64_t)u * kBlock * kVec;
-            acc += hash_word(W[u].x & 0xFFFFu, i | kTagB) + hash_word(W[u].x >> 16, (i + 1) | kTagB) +
-                   hash_word(W[u].y & 0xFFFFu, (i + 2) | kTagB) + hash_word(W[u].y >> 16, (i + 3) | kTagB);
+            const uint32_t o = u * kBlock * kVec;
+            acc += ix.template hash<kTagB>(W[u].x & 0xFFFFu, o) + ix.template hash<kTagB>(W[u].x >> 16, o + 1) +
+                   ix.template hash<kTagB>(W[u].y & 0xFFFFu, o + 2) + ix.template hash<kTagB>(W[u].y >> 16, o + 3);
         }
         return acc;
     } else {
@@ -306,8 +364,9 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
         for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
             for (int j = 0; j < kVec; ++j) {
-                const uint64_t i = lane_idx + (uint64_t)u * kBlock * kVec + j;
-                acc += hash_word(P[u][j], i) + hash_word(Mo[u][j], i | kTagM) + hash_word(V[u][j], i | kTagV);
+                const uint32_t o = u * kBlock * kVec + j;
+                acc += ix.template hash<kTagP>(P[u][j], o) + ix.template hash<kTagM>(Mo[u][j], o) +
+                       ix.template hash<kTagV>(V[u][j], o);
             }
         }
         return acc;
@@ -338,15 +397,15 @@ __device__ __forceinline__ uint64_t do_scalar(const ArraysBf16& a, uint64_t e, c
         a.m[e] = (uint16_t)m;
         a.v[e] = (uint16_t)v;
     }
-    return hash_word(p, idx) + hash_word(m, idx | kTagM) + hash_word(v, idx | kTagV);
+    return hash_word<kTagP>(p, idx) + hash_word<kTagM>(m, idx) + hash_word<kTagV>(v, idx);
 }
 
-template <Mode M>
+template <Mode M, typename Ix>
 __device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0, const StepScalars& sc) {
     constexpr int kRows = kTile / (kBlock * 8);
     constexpr uint32_t kRowBytes = kBlock * 16;
     const uint32_t lane = threadIdx.x * 16;
-    const uint64_t lane_idx = a.goff + e0 + threadIdx.x * 8;
+    const Ix ix(a.goff + e0, threadIdx.x * 8);  // word k of this lane: index + k
     const auto rp = tile_rsrc(a.p + e0, kTile * 2);
     const auto rm = tile_rsrc(a.m + e0, kTile * 2);
     const auto rv = tile_rsrc(a.v + e0, kTile * 2);
@@ -386,10 +445,10 @@ __device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0
     for (int r = 0; r < kRows; ++r) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint64_t i = lane_idx + (uint64_t)r * kBlock * 8 + 2 * j;
-            acc += hash_word(P[r][j] & 0xFFFFu, i) + hash_word(P[r][j] >> 16, i + 1) +
-                   hash_word(Mo[r][j] & 0xFFFFu, i | kTagM) + hash_word(Mo[r][j] >> 16, (i + 1) | kTagM) +
-                   hash_word(V[r][j] & 0xFFFFu, i | kTagV) + hash_word(V[r][j] >> 16, (i + 1) | kTagV);
+            const uint32_t o = r * kBlock * 8 + 2 * j;
+            acc += ix.template hash<kTagP>(P[r][j] & 0xFFFFu, o) + ix.template hash<kTagP>(P[r][j] >> 16, o + 1) +
+                   ix.template hash<kTagM>(Mo[r][j] & 0xFFFFu, o) + ix.template hash<kTagM>(Mo[r][j] >> 16, o + 1) +
+                   ix.template hash<kTagV>(V[r][j] & 0xFFFFu, o) + ix.template hash<kTagV>(V[r][j] >> 16, o + 1);
         }
     }
     return acc;
@@ -419,7 +478,16 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
     const uint64_t e0 = seg_first + (tile - bt.tile_begin[seg]) * (uint64_t)kTile;
     uint64_t acc = 0;
     if (bt.vec_ok[seg] && e0 + kTile <= seg_end) {
-        acc = do_tile_vec<M>(a, e0, sc);
+        // The short index form for tiles that do not cross a multiple of
+        // 2^32 (a uniform branch: at most one tile in 2^20 takes the other);
+        // the binary32 commits are bound by HBM, not by VALU issue, and keep
+        // the plain form (the short one measured 0.3% slower there, with one
+        // more wave per SIMD resident).
+        if (!kCommits<M> && same_high_half(a.goff + e0, kTile)) {
+            acc = do_tile_vec<M, IndexHi32>(a, e0, sc);
+        } else {
+            acc = do_tile_vec<M, IndexAny>(a, e0, sc);
+        }
     } else {
         const uint64_t e1 = (e0 + kTile < seg_end) ? e0 + kTile : seg_end;
         for (uint64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
@@ -434,14 +502,25 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
     }
 }
 
+// Waves per SIMD a kernel must be able to keep resident (caps its VGPRs).
+// The two standalone digests are bound by VALU issue and keep the full
+// eight waves per SIMD (the short index form would otherwise take the state
+// digest to 66 VGPRs and seven waves).  The BF16-state commit measured
+// fastest unbounded (88 VGPRs, five waves): capped at eight waves it spills,
+// at six or seven it is 0.5% slower.
 template <Mode M>
-__global__ __launch_bounds__(kBlock) void tile_kernel(Arrays a, Batch bt) {
+constexpr unsigned kMinWavesPerSimd = (M == Mode::StateDigest || M == Mode::DigestBf16State) ? 8u : 1u;
+
+template <Mode M>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kMinWavesPerSimd<M>)))
+void tile_kernel(Arrays a, Batch bt) {
     __shared__ uint64_t lds[kBlock / 64];
     tile_body<M>(a, bt, lds);
 }
 
 template <Mode M>
-__global__ __launch_bounds__(kBlock) void tile_kernel_bf16(ArraysBf16 a, Batch bt) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kMinWavesPerSimd<M>)))
+void tile_kernel_bf16(ArraysBf16 a, Batch bt) {
     __shared__ uint64_t lds[kBlock / 64];
     tile_body<M>(a, bt, lds);
 }

@@ -197,6 +197,37 @@ def test_global_index_edges(goff):
     assert e.value.code == pk.PACT_ERANGE
 
 
+@pytest.mark.parametrize("goff", [0, 2 ** 32 - 5096, 2 ** 33 - 7000, 2 ** 56 - 3 * 4096 - 123])
+def test_every_digest_across_index_halves(goff):
+    """Each digesting kernel (commit, state digest, bf16 digest, BF16-state
+    commit and digest) on whole tiles that sit below, across and above a
+    multiple of 2^32, and at the top of the index range: the vector path
+    hashes a tile whose indices share their upper 32 bits in a shorter form
+    than one that crosses such a multiple, and both must give the oracle's
+    digest."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    n = 3 * 4096 + 123  # three whole tiles and a ragged tail
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    sh = make_shard(p, g, m, v, goff)
+    d_gpu = pk.to_u64(pk.adamw_commit(sh, 5, g_hyper(H)))[0]
+    b = np.zeros(n, np.uint16)
+    assert d_gpu == oracle.commit_and_digest(p, g, m, v, b, o_hyper(H), 5, goff)
+    _compare_full(sh, p, m, v, b)
+    assert pk.to_u64(pk.shard_digest(sh))[0] == oracle.state_digest(p, m, v, goff)
+    assert pk.to_u64(pk.bf16_digest(sh))[0] == oracle.bf16_digest(b, goff)
+    pb, gb, mb, vb = _bf16_arrays(w, 0, n)
+    t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (pb, gb, mb, vb)]
+    sh16 = pk.ShardBf16(*t, global_offset=goff)
+    got = pk.to_u64(pk.adamw_commit_bf16(sh16, 5, g_hyper(H)))[0]
+    assert got == oracle.commit_and_digest_bf16(pb, gb, mb, vb, o_hyper(H), 5, goff)
+    for name, tt, ref in (("param", sh16.param, pb), ("exp_avg", sh16.exp_avg, mb), ("exp_avg_sq", sh16.exp_avg_sq, vb)):
+        assert_bitwise(name, host(tt).view(np.uint16), ref)
+    assert pk.to_u64(pk.shard_digest_bf16(sh16))[0] == oracle.state_digest_bf16(pb, mb, vb, goff)
+
+
 def test_multi_segment_shrunken_mistral():
     """Real Mistral tensor roles at a small size with padding, four hyper
     sets (norms without decay, lm_head with its own beta2): per-segment
