@@ -260,9 +260,8 @@ def main():
         print(json.dumps(record_traffic(args.workload, *args.record_traffic)))
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the commit of a "
-              "rank's shard needs no communication, and sharding across GPUs is not part of this build.",
-              file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}): the commit of a rank's shard "
+              "needs no communication, and the library has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import torch
