@@ -300,7 +300,7 @@ class ShardArena:
     spacing: bytes between array starts (default ARENA_SPACING = 44 GiB, at
     least the largest array).  The pool holds 4 * spacing + the bf16 array.
     Among even spacings of 24-60 GiB, 44, 56, 58 and 60 GiB measured about 1%
-    faster than 36-42, 48 and 52 GiB on two boxes; 44 GiB is the smallest of
+    faster than 36-42, 48 and 52 GiB on two MI355X GPUs; 44 GiB is the smallest of
     the fast ones.
     """
 
