@@ -406,10 +406,24 @@ def shard_digest_bf16(shard: ShardBf16) -> torch.Tensor:
     return shard.digest
 
 
+def _result_slots(shard, out: Optional[torch.Tensor]) -> torch.Tensor:
+    """``out`` checked as a destination for the shard's result slots (int64
+    device tensor on the shard's GPU, contiguous, at least ``shard.slots``
+    long), or a fresh zeroed one."""
+    if out is None:
+        return torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
+    if not isinstance(out, torch.Tensor) or out.dtype != torch.int64:
+        raise TypeError("out must be an int64 torch tensor")
+    if out.device != shard.device:
+        raise ValueError(f"out is on {out.device}, the shard on {shard.device}")
+    if not out.is_contiguous() or out.numel() < shard.slots:
+        raise ValueError(f"out must be contiguous with at least {shard.slots} elements")
+    return out
+
+
 def grad_guard(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Count the gradient elements that are not +0.0 (per segment and total)."""
-    if out is None:
-        out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
+    out = _result_slots(shard, out)
     with torch.cuda.device(shard.device):
         rc = _lib().pact_grad_guard(ctypes.byref(shard._c()), out.data_ptr())
     _note_workspace(shard, rc)
@@ -428,8 +442,7 @@ def shard_digest(shard: Shard) -> torch.Tensor:
 
 def bf16_digest(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Digest (tag 3) of the bf16 copy, into ``out`` (allocated if None)."""
-    if out is None:
-        out = torch.zeros(shard.slots, dtype=torch.int64, device=shard.device)
+    out = _result_slots(shard, out)
     with torch.cuda.device(shard.device):
         rc = _lib().pact_bf16_digest(ctypes.byref(shard._c()), out.data_ptr())
     _note_workspace(shard, rc)
@@ -438,8 +451,16 @@ def bf16_digest(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tenso
 
 
 def stream_probe(i0, i1, i2, i3, o0, o2, o3, oh) -> None:
-    """30-byte/element streaming probe (measurement support)."""
+    """30-byte/element streaming probe (measurement support): reads the four
+    fp32 tensors i0..i3, writes o0, o2, o3 (fp32) and oh (16-bit); all on one
+    GPU, contiguous, with the same element count.  Outputs may be the inputs
+    (in place)."""
+    if not isinstance(i0, torch.Tensor):
+        raise TypeError("i0 must be a torch tensor")
     n = i0.numel()
+    for name, t in (("i0", i0), ("i1", i1), ("i2", i2), ("i3", i3), ("o0", o0), ("o2", o2), ("o3", o3)):
+        _dev_tensor(t, (torch.float32,), name, n, i0.device)
+    _dev_tensor(oh, (torch.int16, torch.bfloat16), "oh", n, i0.device)
     with torch.cuda.device(i0.device):
         rc = _lib().pact_stream_probe(i0.data_ptr(), i1.data_ptr(), i2.data_ptr(), i3.data_ptr(),
                                       o0.data_ptr(), o2.data_ptr(), o3.data_ptr(), oh.data_ptr(), n,

@@ -492,7 +492,7 @@ int pact_stream_probe(const float* in0, const float* in1, const float* in2, cons
         !aligned(out2, 16) || !aligned(out3, 16) || !aligned(out_half, 8)) {
         return PACT_EALIGN;
     }
-    if ((n + pact::kTile - 1) / pact::kTile > (uint64_t)INT32_MAX) return PACT_ERANGE;
+    if ((n + pact::kTile - 1) / pact::kTile > (uint64_t)(UINT32_MAX / pact::kBlock)) return PACT_ERANGE;
     hipError_t e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n,
                                       static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail_hip(e);
@@ -505,7 +505,7 @@ const char* pact_strerror(int code) {
         case PACT_EINVAL: return "invalid argument";
         case PACT_EALIGN: return "misaligned pointer";
         case PACT_EOVERLAP: return "buffers overlap";
-        case PACT_ERANGE: return "index range reaches the digest tag bits (2^56) or wraps";
+        case PACT_ERANGE: return "index range reaches the digest tag bits (2^56), wraps, or exceeds one launch grid";
         case PACT_EHIP: return "HIP call failed";
         default: return "unknown error";
     }

@@ -216,6 +216,8 @@ def test_binding_refuses_cpu_tensors():
     t = torch.zeros(16)
     with pytest.raises(TypeError):
         pk.Shard(t, t, t, t, torch.zeros(16, dtype=torch.int16))
+    with pytest.raises(TypeError):
+        pk.stream_probe(t, t, t, t, t, t, t, torch.zeros(16, dtype=torch.int16))
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):

@@ -598,6 +598,33 @@ def test_stream_probe_moves_the_bytes():
     assert torch.equal(h, top)
 
 
+def test_binding_checks_result_and_probe_tensors():
+    """Destinations for result slots and the probe's tensors are checked
+    before anything reaches the library."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["tiny"]
+    p, g, m, v = wl.arrays_host(w, 0, 4096)
+    sh = make_shard(p, g, m, v, 0)
+    for bad in (torch.zeros(1, dtype=torch.int64),                      # on the host
+                torch.zeros(1, dtype=torch.float64, device="cuda"),     # wrong dtype
+                torch.zeros(0, dtype=torch.int64, device="cuda"),       # too short
+                torch.zeros(4, dtype=torch.int64, device="cuda")[::2]):  # not contiguous
+        with pytest.raises((TypeError, ValueError)):
+            pk.grad_guard(sh, out=bad)
+        with pytest.raises((TypeError, ValueError)):
+            pk.bf16_digest(sh, out=bad)
+    f = torch.zeros(4096, device="cuda")
+    h = torch.zeros(4096, dtype=torch.int16, device="cuda")
+    with pytest.raises(ValueError):
+        pk.stream_probe(f, f, f, torch.zeros(4092, device="cuda"), f, f, f, h)
+    with pytest.raises(TypeError):
+        pk.stream_probe(f, f, f, f, f, f, f, torch.zeros(4096, device="cuda"))
+    ok = torch.zeros(1, dtype=torch.int64, device="cuda")
+    assert pk.grad_guard(sh, out=ok) is ok
+
+
 def test_shard_arena_layout():
     """The placement-aware arena: five arrays at `spacing` strides in one
     pool, gaps usable through take(), and a commit on it equal to the oracle."""
