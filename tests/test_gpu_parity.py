@@ -252,6 +252,56 @@ def test_multi_segment_shrunken_mistral():
     del torch
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_random_segment_tables(seed):
+    """Seeded random segment tables: lengths from empty to several tiles (one
+    element, unaligned, exact multiples of a tile), gaps of padding between
+    segments, random hyper indices over three hyper sets, a random global
+    offset below 2^40, sometimes more segments than one launch carries.  The
+    commit (every per-segment digest, the total and every output, padding
+    untouched), the standalone digest and the zero-grad commit with the
+    guard all match the oracle."""
+    pk = _pk()
+    rng = np.random.default_rng(1000 + seed)
+    hypers = [dict(H), dict(H, lr=1.5e-4, weight_decay=0.0), dict(H, beta2=0.99, eps=1e-6)]
+    nseg = int(rng.integers(1, 80))
+    segs, off = [], int(rng.integers(0, 9))
+    for _ in range(nseg):
+        ln = int(rng.choice([0, 1, 3, 7, 128, 4095, 4096, 4097, 8192, int(rng.integers(1, 20000))]))
+        segs.append((off, ln, int(rng.integers(0, 3))))
+        off += ln + int(rng.choice([0, 0, 1, 2, 5, 128, 4096]))
+    n = off + int(rng.integers(0, 7))
+    goff = int(rng.integers(0, 1 << 40))
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    sh = make_shard(p, g, m, v, goff, segments=segs, hypers=hypers)
+    sh.param_bf16.fill_(0x3C3C)
+    p0, m0, v0 = p.copy(), m.copy(), v.copy()
+    got = pk.to_u64(pk.adamw_commit(sh, 7))
+    b = np.full(n, 0x3C3C, np.uint16)
+    per, total = oracle.commit_segments(p, g, m, v, b, segs, [o_hyper(h) for h in hypers], 7, goff)
+    assert got == per + [total]
+    _compare_full(sh, p, m, v, b)
+    covered = np.zeros(n, bool)
+    for o, ln, _ in segs:
+        covered[o:o + ln] = True
+    assert np.array_equal(p[~covered].view(np.uint32), p0[~covered].view(np.uint32))
+    assert np.array_equal(m[~covered].view(np.uint32), m0[~covered].view(np.uint32))
+    assert np.array_equal(v[~covered].view(np.uint32), v0[~covered].view(np.uint32))
+    sd_per, sd_total = oracle.segment_digests(p, m, v, segs, goff)
+    assert pk.to_u64(pk.shard_digest(sh)) == sd_per + [sd_total]
+    got_z = pk.to_u64(pk.adamw_commit(sh, 8, zero_grad=True))
+    per_z, total_z = oracle.commit_segments(p, g, m, v, b, segs, [o_hyper(h) for h in hypers], 8, goff)
+    assert got_z == per_z + [total_z]
+    _compare_full(sh, p, m, v, b, "zero-grad ")
+    g_after = host(sh.grad)
+    want_g = g.copy()
+    want_g[covered] = 0.0
+    assert np.array_equal(g_after.view(np.uint32), want_g.view(np.uint32))
+    guard = pk.to_u64(pk.grad_guard(sh))
+    assert guard == [0] * (len(segs) + 1)
+
+
 def test_many_segments_span_several_launches():
     """More segments than one launch carries (32), with empty, one-element,
     unaligned and ragged segments and gaps between them."""
