@@ -252,6 +252,20 @@ def test_multi_segment_shrunken_mistral():
     del torch
 
 
+def _random_segment_table(seed):
+    """(segments, numel, global offset, hyper dicts) drawn from `seed`."""
+    rng = np.random.default_rng(seed)
+    hypers = [dict(H), dict(H, lr=1.5e-4, weight_decay=0.0), dict(H, beta2=0.99, eps=1e-6)]
+    nseg = int(rng.integers(1, 80))
+    segs, off = [], int(rng.integers(0, 9))
+    for _ in range(nseg):
+        ln = int(rng.choice([0, 1, 3, 7, 128, 4095, 4096, 4097, 8192, int(rng.integers(1, 20000))]))
+        segs.append((off, ln, int(rng.integers(0, 3))))
+        off += ln + int(rng.choice([0, 0, 1, 2, 5, 128, 4096]))
+    n = off + int(rng.integers(0, 7))
+    return segs, n, int(rng.integers(0, 1 << 40)), hypers
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_random_segment_tables(seed):
     """Seeded random segment tables: lengths from empty to several tiles (one
@@ -262,16 +276,7 @@ def test_random_segment_tables(seed):
     untouched), the standalone digest and the zero-grad commit with the
     guard all match the oracle."""
     pk = _pk()
-    rng = np.random.default_rng(1000 + seed)
-    hypers = [dict(H), dict(H, lr=1.5e-4, weight_decay=0.0), dict(H, beta2=0.99, eps=1e-6)]
-    nseg = int(rng.integers(1, 80))
-    segs, off = [], int(rng.integers(0, 9))
-    for _ in range(nseg):
-        ln = int(rng.choice([0, 1, 3, 7, 128, 4095, 4096, 4097, 8192, int(rng.integers(1, 20000))]))
-        segs.append((off, ln, int(rng.integers(0, 3))))
-        off += ln + int(rng.choice([0, 0, 1, 2, 5, 128, 4096]))
-    n = off + int(rng.integers(0, 7))
-    goff = int(rng.integers(0, 1 << 40))
+    segs, n, goff, hypers = _random_segment_table(1000 + seed)
     w = wl.WORKLOADS["mistral7b_shard16"]
     p, g, m, v = wl.arrays_host(w, 0, n)
     sh = make_shard(p, g, m, v, goff, segments=segs, hypers=hypers)
@@ -821,3 +826,35 @@ def test_bf16_state_segments():
     assert got == per + [sum(per) & M64]
     for name, tt, ref in (("param", sh.param, p), ("exp_avg", sh.exp_avg, m), ("exp_avg_sq", sh.exp_avg_sq, v)):
         assert_bitwise(name, host(tt).view(np.uint16), ref)
+@pytest.mark.parametrize("seed", range(3))
+def test_bf16_state_random_segment_tables(seed):
+    """BF16 state over seeded random segment tables (as for binary32 state):
+    per-segment digests, their sum, every output, padding untouched, and the
+    standalone digest."""
+    import torch
+
+    pk = _pk()
+    segs, n, goff, hypers = _random_segment_table(2000 + seed)
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    p, g, m, v = _bf16_arrays(w, 0, n)
+    t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (p, g, m, v)]
+    sh = pk.ShardBf16(*t, global_offset=goff, segments=segs, hypers=[g_hyper(h) for h in hypers])
+    got = pk.to_u64(pk.adamw_commit_bf16(sh, 9))
+    p0, m0, v0 = p.copy(), m.copy(), v.copy()
+    per = []
+    for o, ln, hi in segs:
+        sl = slice(o, o + ln)
+        pp, gg, mm, vv = (a[sl].copy() for a in (p, g, m, v))
+        per.append(oracle.commit_and_digest_bf16(pp, gg, mm, vv, o_hyper(hypers[hi]), 9, goff + o))
+        p[sl], m[sl], v[sl] = pp, mm, vv
+    assert got == per + [sum(per) & M64]
+    for name, tt, ref in (("param", sh.param, p), ("exp_avg", sh.exp_avg, m), ("exp_avg_sq", sh.exp_avg_sq, v)):
+        assert_bitwise(name, host(tt).view(np.uint16), ref)
+    covered = np.zeros(n, bool)
+    for o, ln, _ in segs:
+        covered[o:o + ln] = True
+    assert np.array_equal(p[~covered], p0[~covered])
+    want = [oracle.state_digest_bf16(p[o:o + ln], m[o:o + ln], v[o:o + ln], goff + o) for o, ln, _ in segs]
+    assert pk.to_u64(pk.shard_digest_bf16(sh)) == want + [sum(want) & M64]
+
+
