@@ -249,3 +249,141 @@ def test_header_is_c99_and_matches_the_binding(tmp_path):
         assert py_fields == c_fields, (name, py_fields, c_fields)
     for code, value in c["codes"].items():
         assert getattr(pk, code) == value, code
+
+
+# ---------------------------------------------------------------------------
+# Seeded fuzz of the argument validation: a random well-formed shard (fake,
+# aligned, disjoint device addresses) with exactly one injected violation of
+# a known kind; the call must report exactly that kind.  Every case is
+# invalid, so nothing is ever enqueued.
+# ---------------------------------------------------------------------------
+_VIOLATIONS = {
+    # name: (expected code, applies to the state digest call too)
+    "null_param": (pk.PACT_EINVAL, True), "null_grad": (pk.PACT_EINVAL, False),
+    "null_bf16": (pk.PACT_EINVAL, False), "null_digest": (pk.PACT_EINVAL, True),
+    "step0": (pk.PACT_EINVAL, False), "bad_hyper": (pk.PACT_EINVAL, False),
+    "no_hyper": (pk.PACT_EINVAL, False), "flags": (pk.PACT_EINVAL, False),
+    "range": (pk.PACT_ERANGE, True), "misalign_m": (pk.PACT_EALIGN, True),
+    "misalign_bf16": (pk.PACT_EALIGN, False), "misalign_digest": (pk.PACT_EALIGN, True),
+    "overlap_arrays": (pk.PACT_EOVERLAP, True), "overlap_digest": (pk.PACT_EOVERLAP, True),
+    "ws_small": (pk.PACT_EINVAL, True), "ws_misalign": (pk.PACT_EALIGN, True),
+    "ws_overlap": (pk.PACT_EOVERLAP, True), "seg_reserved": (pk.PACT_EINVAL, True),
+    "seg_order": (pk.PACT_EINVAL, True), "seg_beyond": (pk.PACT_EINVAL, True),
+    "seg_hyper_index": (pk.PACT_EINVAL, False), "seg_bad_hyper": (pk.PACT_EINVAL, False),
+    "seg_count0": (pk.PACT_EINVAL, True),
+}
+_SEG_ONLY = {"seg_reserved", "seg_order", "seg_beyond", "seg_hyper_index", "seg_bad_hyper", "seg_count0"}
+_FLAT_ONLY = {"bad_hyper", "no_hyper"}
+
+
+def _random_hyper(rng):
+    return _CHyper(float(rng.uniform(0, 1e-2)), float(rng.uniform(0, 0.999)), float(rng.uniform(0, 0.9999)),
+                   float(rng.uniform(1e-12, 1e-3)), float(rng.uniform(0, 0.5)))
+
+
+def _fuzz_case(rng, violation):
+    import numpy as np
+
+    n = int(rng.integers(1, 1 << 20))
+    s = _CShard()
+    arr = [BASE + k * SPAN + 16 * int(rng.integers(0, 1 << 16)) for k in range(5)]
+    s.param, s.grad, s.exp_avg, s.exp_avg_sq, s.param_bf16 = arr
+    s.numel = n
+    s.global_offset = int(rng.integers(0, (1 << 56) - n))
+    s.digest_dev = BASE + 5 * SPAN + 8 * int(rng.integers(0, 1 << 16))
+    keep = []
+    segmented = violation in _SEG_ONLY or (violation not in _FLAT_ONLY and rng.random() < 0.5)
+    if segmented:
+        k = int(rng.integers(2, 40))
+        cuts = np.sort(rng.integers(0, n + 1, size=2 * k))
+        segs = [[int(cuts[2 * i]), int(cuts[2 * i + 1] - cuts[2 * i]), 0, 0] for i in range(k)]
+        hyps = [_random_hyper(rng) for _ in range(int(rng.integers(1, 4)))]
+        for sg in segs:
+            sg[2] = int(rng.integers(0, len(hyps)))
+        if violation == "seg_reserved":
+            segs[int(rng.integers(0, k))][3] = 1
+        elif violation == "seg_order":
+            i = int(rng.integers(0, k - 1))
+            while segs[i] == segs[i + 1]:  # swapping equal entries changes nothing
+                segs[i + 1][0] += 1
+                segs[i + 1][1] = max(0, segs[i + 1][1] - 1)
+            segs[i], segs[i + 1] = segs[i + 1], segs[i]
+        elif violation == "seg_beyond":
+            segs[-1][1] = n - segs[-1][0] + int(rng.integers(1, 1000))
+        elif violation == "seg_hyper_index":
+            segs[int(rng.integers(0, k))][2] = len(hyps)
+        elif violation == "seg_bad_hyper":
+            hyps[segs[int(rng.integers(0, k))][2]] = _CHyper(3e-4, 1.0, 0.95, 1e-8, 0.1)
+        table = (_CSegment * k)(*[_CSegment(*sg) for sg in segs])
+        htable = (_CHyper * len(hyps))(*hyps)
+        keep += [table, htable]
+        s.segs = ctypes.cast(table, ctypes.POINTER(_CSegment))
+        s.num_segs = 0 if violation == "seg_count0" else k
+        s.hypers = ctypes.cast(htable, ctypes.POINTER(_CHyper))
+        s.num_hypers = len(hyps)
+        hyper = None
+    else:
+        hyper = _random_hyper(rng)
+        if violation == "bad_hyper":
+            bad = [("lr", -1e-3), ("beta1", 1.0), ("beta2", float("nan")), ("eps", 0.0), ("weight_decay", -0.1)]
+            name, val = bad[int(rng.integers(0, len(bad)))]
+            setattr(hyper, name, val)
+    if rng.random() < 0.5 or violation.startswith("ws_"):
+        need = pk._lib().pact_workspace_bytes(ctypes.byref(s))
+        s.workspace = BASE + 6 * SPAN + 8 * int(rng.integers(0, 1 << 16))
+        s.workspace_bytes = need + 8 * int(rng.integers(0, 4))
+        if violation == "ws_small":
+            s.workspace_bytes = need - 8
+        elif violation == "ws_misalign":
+            s.workspace += 4
+        elif violation == "ws_overlap":
+            s.workspace = s.exp_avg + 8 * int(rng.integers(0, n // 2 + 1))
+    if violation == "null_param":
+        s.param = None
+    elif violation == "null_grad":
+        s.grad = None
+    elif violation == "null_bf16":
+        s.param_bf16 = None
+    elif violation == "null_digest":
+        s.digest_dev = None
+    elif violation == "range":
+        s.global_offset = (1 << 56) - n + int(rng.integers(1, 1 << 20))
+    elif violation == "misalign_m":
+        s.exp_avg += int(rng.integers(1, 4))
+    elif violation == "misalign_bf16":
+        s.param_bf16 += 1
+    elif violation == "misalign_digest":
+        s.digest_dev += 4
+    elif violation == "overlap_arrays":
+        s.exp_avg_sq = s.param + 4 * int(rng.integers(0, n))
+    elif violation == "overlap_digest":
+        s.digest_dev = s.exp_avg + 8 * int(rng.integers(0, n // 2))  # an array both calls read
+    step = 0 if violation == "step0" else int(rng.integers(1, 1 << 20))
+    flags = (1 << int(rng.integers(2, 32))) if violation == "flags" else int(rng.integers(0, 4))
+    if violation == "no_hyper":
+        hyper = None
+    return s, step, hyper, flags, keep
+
+
+def test_validation_fuzz():
+    """800 seeded cases, each a well-formed shard with one injected
+    violation: the commit reports exactly that violation's code, and so does
+    the state digest for the violations that concern it."""
+    import numpy as np
+    import torch
+
+    if torch.cuda.is_available():
+        pytest.skip("host-only test: fake device addresses")
+    lib = pk._lib()
+    rng = np.random.default_rng(4242)
+    names = sorted(_VIOLATIONS)
+    for case in range(800):
+        violation = names[case % len(names)]
+        s, step, hyper, flags, keep = _fuzz_case(rng, violation)
+        want, digest_too = _VIOLATIONS[violation]
+        got = lib.pact_adamw_commit_ex(ctypes.byref(s), step, ctypes.byref(hyper) if hyper is not None else None,
+                                       flags)
+        assert got == want, (case, violation, got)
+        if digest_too:
+            assert lib.pact_shard_digest(ctypes.byref(s)) == want, (case, violation)
+        del keep
