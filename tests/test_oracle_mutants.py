@@ -1,17 +1,23 @@
 """Mutation check of the oracle's pins (no GPU): each case plants one
-plausible mistake in a copy of oracle.c (a dropped term, a wrong sign, a
-swapped operand, an off-by-one, a wrong constant, a different rounding),
-builds it, and runs the pin suite against it.  Every mutant must fail at
-least one pin; the unmutated copy must pass them all."""
+plausible mistake in a copy of the oracle -- in oracle.c (a dropped term, a
+wrong sign, a swapped operand, an off-by-one, a wrong constant, a different
+rounding) or in the segment walkers of oracle/__init__.py (a segment given
+another segment's hyperparameters, a segment digested at the wrong flat
+index) -- and runs the pin suite against it.  Only tests/test_oracle_pins.py
+runs: the stored oracle-written digests under tests/golden/ would trip on
+almost any change and so cannot show that the pins themselves bite.  Every
+mutant must fail at least one pin; the unmutated copies must pass them all."""
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "oracle.c")
-PIN_FILES = ["tests/test_oracle_pins.py", "tests/test_golden.py"]
+PIN_FILES = ["tests/test_oracle_pins.py"]
+PY_SRC = os.path.join(ROOT, "oracle", "__init__.py")
 FLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fno-math-errno",
          "-fexcess-precision=standard", "-fPIC", "-shared"]
 
@@ -62,21 +68,80 @@ def _build(tmp_path, text, name):
     return lib
 
 
-def _pins_pass(lib):
-    env = dict(os.environ, PACT_ORACLE_LIB=str(lib))
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PIN_FILES],
-                       cwd=ROOT, env=env, capture_output=True, text=True)
+def _pins_pass(basetemp, lib=None, root=ROOT):
+    env = dict(os.environ)
+    if lib is not None:
+        env["PACT_ORACLE_LIB"] = str(lib)
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        f"--basetemp={basetemp}", *PIN_FILES],
+                       cwd=root, env=env, capture_output=True, text=True)
     return r.returncode == 0, r.stdout[-400:]
 
 
-def test_unmutated_copy_passes(tmp_path):
-    ok, out = _pins_pass(_build(tmp_path, open(SRC).read(), "clean"))
+# (name, text to find, replacement); each text must occur in oracle/__init__.py
+PY_MUTANTS = [
+    ("walker gives every segment the first hyper set", "bf16[sl], hypers[hi], step,", "bf16[sl], hypers[0], step,"),
+    ("walker digests each segment at the shard start", "global_offset + off)\n        per.append(d)",
+     "global_offset)\n        per.append(d)"),
+    ("walker ignores the shard's global offset", "global_offset + off)\n        per.append(d)",
+     "off)\n        per.append(d)"),
+    ("read-only walker drops the segment offset", "v[sl], global_offset + off))",
+     "v[sl], global_offset))"),
+]
+
+
+def _tree_with_oracle_init(tmp_path, init_text):
+    """A copy of the repository made of symlinks, except oracle/__init__.py,
+    which holds `init_text`: the pins then import that oracle module."""
+    root = tmp_path / "root"
+    root.mkdir()
+    for name in os.listdir(ROOT):
+        if name in ("oracle", ".git", "_work", "gpurun_out", ".pytest_cache", "__pycache__"):
+            continue
+        os.symlink(os.path.join(ROOT, name), root / name)
+    od = root / "oracle"
+    od.mkdir()
+    for name in os.listdir(os.path.join(ROOT, "oracle")):
+        if name not in ("__init__.py", "__pycache__"):
+            os.symlink(os.path.join(ROOT, "oracle", name), od / name)
+    (od / "__init__.py").write_text(init_text)
+    return root
+
+
+# every case: (id, kind, text to find or None, replacement)
+CASES = ([("clean oracle.c", "c", None, None)] + [(n, "c", f, r) for n, f, r in MUTANTS]
+         + [("clean walker", "py", None, None)] + [(n, "py", f, r) for n, f, r in PY_MUTANTS])
+
+
+@pytest.fixture(scope="module")
+def outcomes(tmp_path_factory):
+    """Runs the pin suite once per case, several cases at a time (each in its
+    own process with its own oracle); returns {id: (pins passed, tail)}."""
+    def run(case):
+        name, kind, find, repl = case
+        src = SRC if kind == "c" else PY_SRC
+        text = open(src).read()
+        if find is not None:
+            if text.count(find) != 1:
+                return None
+            text = text.replace(find, repl)
+        d = tmp_path_factory.mktemp("case")
+        if kind == "c":
+            return _pins_pass(d / "pytest", lib=_build(d, text, "oracle_case"))
+        return _pins_pass(d / "pytest", root=_tree_with_oracle_init(d, text))
+
+    with ThreadPoolExecutor(max(1, min(6, os.cpu_count() or 1))) as ex:
+        return dict(zip([c[0] for c in CASES], ex.map(run, CASES)))
+
+
+@pytest.mark.parametrize("name", ["clean oracle.c", "clean walker"])
+def test_unmutated_copy_passes(outcomes, name):
+    ok, out = outcomes[name]
     assert ok, out
 
 
-@pytest.mark.parametrize("name,find,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(tmp_path, name, find, repl):
-    text = open(SRC).read()
-    assert text.count(find) == 1, f"mutation site not unique: {name}"
-    ok, out = _pins_pass(_build(tmp_path, text.replace(find, repl), "mutant"))
+@pytest.mark.parametrize("name", [c[0] for c in CASES if c[2] is not None])
+def test_mutant_is_caught(outcomes, name):
+    assert outcomes[name] is not None, f"mutation site not unique: {name}"
+    ok, out = outcomes[name]
     assert not ok, f"the pins did not catch: {name}"

@@ -396,6 +396,95 @@ def test_segments_sum_and_padding_excluded():
     assert per3 == per and total3 == total
 
 
+def _padding_runs(segments, numel):
+    """[start, end) runs of the flat layout that no segment covers."""
+    runs, at = [], 0
+    for off, ln, _ in segments:
+        if off > at:
+            runs.append((at, off))
+        at = off + ln
+    if at < numel:
+        runs.append((at, numel))
+    return runs
+
+
+def test_segment_walker_uses_each_segments_hypers_and_position():
+    """Pin of the multi-segment walker (per-tensor W, M, V of Sec. III-A, eq. 2,
+    each tensor with its own AdamW settings) against facts that do not go
+    through it.  At t = 1 from m = v = 0 every element of segment s must show
+    its own role's closed-form first step: m' = f32(omb1 g) and
+    v' = f32(omb2 f32(g g)) bit for bit (lm_head has beta2 0.99, the others
+    0.95), and p' inside the exact first-order bound of
+    P = p (1 - lr wd) - lr g / (|g| + eps) with the segment's lr and wd
+    (embed and lm_head lr 1.5e-4, norms wd 0).  Padding keeps its bits.  The
+    digests must satisfy the flat identity: the state digest of the whole
+    committed array at the global offset (no walker involved) equals the
+    walkers' total plus the digests of the padding runs, for the committing
+    and for the read-only walker."""
+    w = wl.shrunken_mistral()
+    roles = {hi for _, _, hi in w.segments}
+    assert roles == set(range(len(w.hypers))), "every role must own a segment"
+    goff = 3 * (1 << 32) + 12345  # a rank whose indices start beyond 2^32
+    p, g, m, v = wl.arrays_host(w)
+    m[:] = 0.0
+    v[:] = 0.0
+    b = np.zeros(w.numel, np.uint16)
+    p0, g0 = p.copy(), g.copy()
+    hypers = [oracle.Hyper(**h) for h in w.hypers]
+    per, total = oracle.commit_segments(p, g, m, v, b, w.segments, hypers, 1, goff)
+
+    covered = np.zeros(w.numel, bool)
+    for off, ln, hi in w.segments:
+        sl = slice(off, off + ln)
+        covered[sl] = True
+        h = w.hypers[hi]
+        lr, wd, eps = f32(h["lr"]), f32(h["weight_decay"]), f32(h["eps"])
+        omb1 = np.float32(1.0 - f32(h["beta1"]))
+        omb2 = np.float32(1.0 - f32(h["beta2"]))
+        gs = g0[sl]
+        assert np.array_equal(m[sl], omb1 * gs), ("m'", off, hi)
+        assert np.array_equal(v[sl], omb2 * (gs * gs)), ("v'", off, hi)
+        g64, p64 = gs.astype(np.float64), p0[sl].astype(np.float64)
+        u = lr * g64 / (np.abs(g64) + eps)
+        P = p64 * (1.0 - lr * wd) - u
+        bound = 0.5 * ulp(p[sl]) + 3 * ULP_EXP * np.abs(p64) + 12 * ULP_EXP * np.abs(u)
+        assert np.all(np.abs(p[sl].astype(np.float64) - P) <= bound), ("p'", off, hi)
+        assert np.array_equal(b[sl], oracle.bf16_rne_bits(p[sl].view(np.uint32))), ("bf16", off, hi)
+    # the checks above tell the roles apart: another role's settings fail them
+    for off, ln, hi in w.segments:
+        other = [k for k in range(len(w.hypers)) if w.hypers[k] != w.hypers[hi]]
+        sl = slice(off, off + ln)
+        for k in other:
+            h = w.hypers[k]
+            lr, wd, eps = f32(h["lr"]), f32(h["weight_decay"]), f32(h["eps"])
+            g64, p64 = g0[sl].astype(np.float64), p0[sl].astype(np.float64)
+            u = lr * g64 / (np.abs(g64) + eps)
+            P = p64 * (1.0 - lr * wd) - u
+            bound = 0.5 * ulp(p[sl]) + 3 * ULP_EXP * np.abs(p64) + 12 * ULP_EXP * np.abs(u)
+            same_p = np.all(np.abs(p[sl].astype(np.float64) - P) <= bound)
+            same_v = np.array_equal(v[sl], np.float32(1.0 - f32(h["beta2"])) * (g0[sl] * g0[sl]))
+            assert not (same_p and same_v), (off, hi, k)
+    pad = ~covered
+    assert pad.any(), "the layout should contain padding"
+    assert np.array_equal(p[pad].view(np.uint32), p0[pad].view(np.uint32))
+    assert not m[pad].view(np.uint32).any() and not v[pad].view(np.uint32).any() and not b[pad].any()
+
+    runs = _padding_runs(w.segments, w.numel)
+    pad_digest = sum(oracle.state_digest(p[a:z], m[a:z], v[a:z], goff + a) for a, z in runs) & M64
+    whole = oracle.state_digest(p, m, v, goff)
+    assert (total + pad_digest) & M64 == whole
+    assert sum(per) & M64 == total
+    per_r, total_r = oracle.segment_digests(p, m, v, w.segments, goff)
+    assert (total_r + pad_digest) & M64 == whole
+    # each segment's digest is the sum of its elements' one-element digests
+    # (spot check on the smallest segments, the norms)
+    for s, (off, ln, hi) in enumerate(w.segments):
+        if ln <= 256:
+            one = sum(oracle.state_digest(p[i:i + 1], m[i:i + 1], v[i:i + 1], goff + i)
+                      for i in range(off, off + ln)) & M64
+            assert one == per[s] == per_r[s], (s, off)
+
+
 # ---------------------------------------------------------------------------
 # workload shapes (the paper's model size)
 # ---------------------------------------------------------------------------
