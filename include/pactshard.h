@@ -31,8 +31,9 @@
  *
  * Memory and ownership.  Every buffer belongs to the caller; the library
  * allocates nothing.  All array pointers are device pointers (HBM).
- * param, exp_avg, exp_avg_sq are read and overwritten in place; grad is only
- * read; param_bf16 is only written.  The five arrays must not overlap each
+ * param, exp_avg, exp_avg_sq are read and overwritten in place; grad is
+ * read (and overwritten with +0.0 only by a commit asked to zero it);
+ * param_bf16 is only written.  The five arrays must not overlap each
  * other or digest_dev.  fp32 arrays need 4-byte and bf16 2-byte alignment;
  * a segment whose start is 16-byte aligned in all four fp32 arrays and 8-byte
  * aligned in the bf16 array runs the vector path, any other segment the
@@ -104,7 +105,8 @@ typedef struct pact_segment {
  * segs and hypers are host pointers read during the call only. */
 typedef struct pact_shard {
     float* param;            /* W: fp32 master weights, numel elements          */
-    const float* grad;       /* fp32 gradient, numel elements                   */
+    float* grad;             /* fp32 gradient, numel elements; written only by  */
+                             /* PACT_COMMIT_ZERO_GRAD, read-only otherwise      */
     float* exp_avg;          /* M: fp32 first moment                            */
     float* exp_avg_sq;       /* V: fp32 second moment                           */
     uint16_t* param_bf16;    /* bf16 working copy of W (bit patterns)           */
@@ -153,8 +155,7 @@ int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hype
  * every committed element of `grad` (4 more bytes per element, 34 in all),
  * so that one call leaves the shard at the boundary the paper admits for
  * in-memory recovery: update committed and flat gradients zeroed (Sec. I;
- * Sec. III-C, phase 2).  `grad` must then be writable device memory (the
- * const in pact_shard does not hold for this call).
+ * Sec. III-C, phase 2).  `grad` must then be writable device memory.
  * PACT_COMMIT_WORKSPACE_CLEAN: the caller vouches that the workspace is clear
  * (zero-filled before its first use, and touched since then only by calls on
  * this stream that returned PACT_OK), so the call skips the launch that
