@@ -82,6 +82,7 @@ extern "C" {
 #define PACT_ERANGE (-4)   /* an index reaches 2^56 (the tag bits): global_offset + numel > 2^56; or the
                             * shard needs more than 2^24 - 1 tiles of 4096 elements (one launch grid) */
 #define PACT_EHIP (-5)     /* a HIP call failed; see pact_last_hip_error() */
+#define PACT_ESCRATCH (-6) /* pact_adamw_commit_static: more segments than its static scratch holds */
 
 /* AdamW hyperparameters.  Valid: lr >= 0, 0 <= beta1 < 1, 0 <= beta2 < 1,
  * eps > 0, weight_decay >= 0, all finite. */
@@ -162,6 +163,26 @@ int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hype
  * clears it; a workspace in any other state gives a wrong digest.  Without a
  * workspace the flag has no effect.  Unknown flag bits are PACT_EINVAL. */
 int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * pact_adamw_commit_ex with the digest partial sums kept in a static device
+ * array inside the library instead of a caller workspace.  The array holds
+ * the lanes of at most PACT_STATIC_MAX_SEGMENTS result slots (2 MiB); each
+ * GPU the library runs on holds its own copy until the process ends.
+ * Inputs and outputs are the caller's, as for pact_adamw_commit_ex;
+ * s->workspace must be NULL.  flags: 0 or PACT_COMMIT_ZERO_GRAD.  A shard
+ * with more than PACT_STATIC_MAX_SEGMENTS segments is PACT_ESCRATCH, found
+ * before anything is enqueued.  The call allocates nothing and calls no
+ * allocating routine; the first call on a device looks up the address of
+ * that device's copy (hipGetSymbolAddress, on the device of `stream`), so
+ * a caller that captures should make one call on each device beforehand.
+ * Every call on a GPU shares that GPU's array: each call clears the part it
+ * uses with a kernel before its tiles run, and calls that overlap in time
+ * on one GPU (concurrent streams, or host threads) race and give wrong
+ * digests. */
+#define PACT_STATIC_MAX_SEGMENTS 512
+int pact_adamw_commit_static(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags);
 
 /* Boundary guard for zero outstanding gradients (Sec. III-C, phase 2):
  * counts the elements of `grad` whose 32-bit pattern is not all zero (-0.0

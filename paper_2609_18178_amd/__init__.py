@@ -23,7 +23,8 @@ from typing import Optional, Sequence, Tuple
 import torch
 
 __all__ = [
-    "Hyper", "Shard", "ShardBf16", "ShardArena", "PactError", "adamw_commit", "adamw_commit_bf16", "grad_guard",
+    "Hyper", "Shard", "ShardBf16", "ShardArena", "PactError", "adamw_commit", "adamw_commit_static",
+    "adamw_commit_bf16", "grad_guard",
     "shard_digest", "shard_digest_bf16", "bf16_digest", "stream_probe",
     "digest_slots", "to_u64", "library_path",
 ]
@@ -33,7 +34,8 @@ library_path = os.path.join(_HERE, "libpactshard.so")
 
 MASK64 = (1 << 64) - 1
 
-PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP = 0, -1, -2, -3, -4, -5
+PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP, PACT_ESCRATCH = 0, -1, -2, -3, -4, -5, -6
+PACT_STATIC_MAX_SEGMENTS = 512
 
 
 class PactError(RuntimeError):
@@ -91,6 +93,8 @@ def _lib():
         lib.pact_adamw_commit.restype = ctypes.c_int
         lib.pact_adamw_commit_ex.argtypes = [P, ctypes.c_uint64, ctypes.POINTER(_CHyper), ctypes.c_uint32]
         lib.pact_adamw_commit_ex.restype = ctypes.c_int
+        lib.pact_adamw_commit_static.argtypes = [P, ctypes.c_uint64, ctypes.POINTER(_CHyper), ctypes.c_uint32]
+        lib.pact_adamw_commit_static.restype = ctypes.c_int
         lib.pact_grad_guard.argtypes = [P, ctypes.c_void_p]
         lib.pact_grad_guard.restype = ctypes.c_int
         PB = ctypes.POINTER(_CShardBf16)
@@ -202,7 +206,7 @@ class Shard:
             self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=self.device)
             self.workspace_clean = True
 
-    def _c(self, digest_out: Optional[torch.Tensor] = None) -> _CShard:
+    def _c(self, digest_out: Optional[torch.Tensor] = None, workspace: bool = True) -> _CShard:
         def ptr(t):
             return None if t is None else t.data_ptr()
 
@@ -216,7 +220,7 @@ class Shard:
             s.hypers = ctypes.cast(self._chypers, ctypes.POINTER(_CHyper))
             s.num_hypers = len(self.hypers)
         s.digest_dev = (digest_out if digest_out is not None else self.digest).data_ptr()
-        ws = getattr(self, "workspace", None)
+        ws = getattr(self, "workspace", None) if workspace else None
         if ws is not None:
             s.workspace, s.workspace_bytes = ws.data_ptr(), ws.numel()
         s.stream = torch.cuda.current_stream(self.device).cuda_stream
@@ -383,6 +387,23 @@ def adamw_commit(shard: Shard, step: int, hyper: Optional[Hyper] = None, zero_gr
                                          ctypes.byref(ch) if ch is not None else None, flags)
     _note_workspace(shard, rc)
     _call("pact_adamw_commit_ex", rc)
+    return shard.digest
+
+
+def adamw_commit_static(shard: Shard, step: int, hyper: Optional[Hyper] = None,
+                        zero_grad: bool = False) -> torch.Tensor:
+    """``adamw_commit`` through the entry point that allocates nothing: the
+    digest partial sums go to the library's static device scratch (at most
+    ``PACT_STATIC_MAX_SEGMENTS`` segments) instead of the shard's workspace.
+    Calls on one GPU share that scratch, so they must not overlap in time."""
+    if shard.segments is None and hyper is None:
+        hyper = Hyper()
+    ch = hyper._c() if hyper is not None else None
+    flags = PACT_COMMIT_ZERO_GRAD if zero_grad else 0
+    with torch.cuda.device(shard.device):
+        rc = _lib().pact_adamw_commit_static(ctypes.byref(shard._c(workspace=False)), int(step),
+                                             ctypes.byref(ch) if ch is not None else None, flags)
+    _call("pact_adamw_commit_static", rc)
     return shard.digest
 
 

@@ -6,7 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
-#include <vector>
+#include <mutex>
 
 #include "launch.h"
 
@@ -107,9 +107,12 @@ struct Span {
     uintptr_t lo, hi;  // [lo, hi)
 };
 
-bool overlaps(const std::vector<Span>& spans) {
-    for (size_t i = 0; i < spans.size(); ++i) {
-        for (size_t j = i + 1; j < spans.size(); ++j) {
+// The buffers of one call: the five arrays, the result slots, the workspace.
+constexpr int kMaxSpans = kSlots + 2;
+
+bool overlaps(const Span* spans, int n) {
+    for (int i = 0; i < n; ++i) {
+        for (int j = i + 1; j < n; ++j) {
             if (spans[i].lo < spans[j].hi && spans[j].lo < spans[i].hi) return true;
         }
     }
@@ -166,11 +169,12 @@ int validate(const View& s, const Uses& use, const uint64_t* out, uint64_t* nslo
         if (!aligned(s.workspace, 8)) return PACT_EALIGN;
         if (s.workspace_bytes < workspace_need(s)) return PACT_EINVAL;
     }
-    std::vector<Span> spans;
+    Span spans[kMaxSpans];
+    int nspans = 0;
     auto add = [&](const void* ptr, uint64_t bytes) {
         if (ptr && bytes) {
             const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
-            spans.push_back({lo, lo + bytes});
+            spans[nspans++] = {lo, lo + bytes};
         }
     };
     for (int k = 0; k < kSlots; ++k) {
@@ -178,10 +182,10 @@ int validate(const View& s, const Uses& use, const uint64_t* out, uint64_t* nslo
     }
     add(out, slots * 8);
     if (s.workspace != nullptr) add(s.workspace, workspace_need(s));
-    for (const Span& sp : spans) {
-        if (sp.hi < sp.lo) return PACT_ERANGE;  // wraps the address space
+    for (int k = 0; k < nspans; ++k) {
+        if (spans[k].hi < spans[k].lo) return PACT_ERANGE;  // wraps the address space
     }
-    if (overlaps(spans)) return PACT_EOVERLAP;
+    if (overlaps(spans, nspans)) return PACT_EOVERLAP;
     *nslots = slots;
     return PACT_OK;
 }
@@ -270,6 +274,42 @@ struct SegWork {
     pact::StepScalars sc;
 };
 
+// The shard's segments as units of work, formed one at a time (a call keeps
+// no table of its own): the whole shard without a segment table, else one
+// per table entry.  `single` and `step` give the scalars when need_hyper.
+struct SegSource {
+    const View* s;
+    const pact_hyper* single;
+    uint64_t step;
+    bool need_hyper;
+
+    size_t count() const { return s->segs ? (size_t)s->num_segs : (s->numel > 0 ? 1 : 0); }
+    SegWork at(size_t k) const {
+        SegWork w{0, s->numel, {}};
+        const pact_hyper* h = single;
+        if (s->segs) {
+            const pact_segment& sg = s->segs[k];
+            w.first = sg.offset;
+            w.count = sg.length;  // empty segments keep their slot (digest 0)
+            h = &s->hypers[sg.hyper_index];
+        }
+        if (need_hyper) w.sc = step_scalars(*h, step);
+        return w;
+    }
+};
+
+// Every segment's hyperparameter index and set, when the mode needs them;
+// PACT_EINVAL before anything is enqueued if one is bad.
+int check_segment_hypers(const View& s) {
+    if (s.segs == nullptr) return PACT_OK;
+    if (s.hypers == nullptr) return PACT_EINVAL;
+    for (uint32_t k = 0; k < s.num_segs; ++k) {
+        const uint32_t hi = s.segs[k].hyper_index;
+        if (hi >= s.num_hypers || !hyper_ok(s.hypers[hi])) return PACT_EINVAL;
+    }
+    return PACT_OK;
+}
+
 bool is_bf16_state(pact::Mode m) { return m == pact::Mode::CommitBf16State || m == pact::Mode::DigestBf16State; }
 
 // Whether a segment starting at element `first` can take the vector path:
@@ -298,7 +338,7 @@ bool vector_ok(pact::Mode mode, const View& s, uint64_t first) {
 
 // workspace_clean: the caller vouches that the workspace lanes are zero (the
 // finish kernel leaves them so), and the clearing launch is skipped.
-int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64_t* out, uint64_t nslots,
+int run(pact::Mode mode, const View& s, const SegSource& work, uint64_t* out, uint64_t nslots,
         bool workspace_clean = false) {
     hipStream_t stream = static_cast<hipStream_t>(s.stream);
     uint64_t* lanes = static_cast<uint64_t*>(s.workspace);
@@ -334,8 +374,9 @@ int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64
     }
 
     const bool per_segment = s.segs != nullptr;
-    for (size_t first = 0; first < work.size(); first += pact::kSegsPerLaunch) {
-        const size_t cnt = std::min<size_t>(pact::kSegsPerLaunch, work.size() - first);
+    const size_t nwork = work.count();
+    for (size_t first = 0; first < nwork; first += pact::kSegsPerLaunch) {
+        const size_t cnt = std::min<size_t>(pact::kSegsPerLaunch, nwork - first);
         pact::Batch b;
         std::memset(&b, 0, sizeof b);
         b.nseg = (uint32_t)cnt;
@@ -343,7 +384,7 @@ int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64
         b.per_segment = per_segment ? 1u : 0u;
         uint64_t tiles = 0;
         for (size_t k = 0; k < cnt; ++k) {
-            const SegWork& w = work[first + k];
+            const SegWork w = work.at(first + k);
             b.tile_begin[k] = tiles;
             tiles += (w.count + pact::kTile - 1) / pact::kTile;
             b.elem_begin[k] = w.first;
@@ -364,46 +405,77 @@ int run(pact::Mode mode, const View& s, const std::vector<SegWork>& work, uint64
     return PACT_OK;
 }
 
-std::vector<SegWork> segment_work(const View& s, const pact_hyper* single, uint64_t step, bool need_hyper,
-                                  int* err) {
-    std::vector<SegWork> work;
-    *err = PACT_OK;
-    if (s.segs == nullptr) {
-        SegWork w{0, s.numel, {}};
-        if (need_hyper) w.sc = step_scalars(*single, step);
-        if (s.numel > 0) work.push_back(w);
-        return work;
-    }
-    if (need_hyper && s.hypers == nullptr) {
-        *err = PACT_EINVAL;
-        return work;
-    }
-    work.reserve(s.num_segs);
-    for (uint32_t k = 0; k < s.num_segs; ++k) {
-        const pact_segment& sg = s.segs[k];
-        SegWork w{sg.offset, sg.length, {}};
-        if (need_hyper) {
-            if (sg.hyper_index >= s.num_hypers || !hyper_ok(s.hypers[sg.hyper_index])) {
-                *err = PACT_EINVAL;
-                return {};
-            }
-            w.sc = step_scalars(s.hypers[sg.hyper_index], step);
+// ---------------------------------------------------------------------------
+// Static scratch of pact_adamw_commit_static: the digest lanes of up to
+// PACT_STATIC_MAX_SEGMENTS result slots in device memory the library holds
+// for the life of the process, one copy per GPU.  In host code `scratch`
+// names a host-side stand-in, not a device address: the device address of
+// each GPU's copy is looked up once per device and only that is used.
+// ---------------------------------------------------------------------------
+constexpr uint64_t kStaticScratchWords = (uint64_t)PACT_STATIC_MAX_SEGMENTS * pact::kLanes * pact::kLaneStride;
+constexpr uint64_t kStaticScratchBytes = kStaticScratchWords * sizeof(uint64_t);
+constexpr int kMaxDevices = 64;
+
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) uint64_t scratch[kStaticScratchWords];
+
+namespace {
+
+// The device address of the GPU's copy of `scratch` for the device `stream`
+// belongs to (the current device for the null stream), looked up with that
+// device current on the first call for it.
+int static_scratch_ptr(void* stream, void** out) {
+    int dev = -1;
+    hipError_t e = stream ? hipStreamGetDevice(static_cast<hipStream_t>(stream), &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e);
+    if (dev < 0 || dev >= kMaxDevices) return PACT_EINVAL;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[dev] == nullptr) {
+        int cur = -1;
+        e = hipGetDevice(&cur);
+        if (e != hipSuccess) return fail_hip(e);
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return fail_hip(e);
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t back = hipSetDevice(cur);
+            if (e == hipSuccess) e = back;
         }
-        work.push_back(w);  // empty segments keep their slot (digest 0)
+        if (e != hipSuccess) return fail_hip(e);
+        if (ptr == nullptr) return fail_hip(hipErrorInvalidSymbol);
+        g_scratch_dev[dev] = ptr;
     }
-    return work;
+    *out = g_scratch_dev[dev];
+    return PACT_OK;
 }
 
-// A commit mode: check step and hyperparameters, validate, enqueue.
-int commit(pact::Mode mode, const View& s, uint64_t step, const pact_hyper* hyper, const Uses& use,
-           bool workspace_clean = false) {
+// A commit mode: check step and hyperparameters, validate, enqueue.  With
+// static_scratch the digest lanes are the library's static array (the
+// caller's workspace must be absent).
+int commit(pact::Mode mode, View s, uint64_t step, const pact_hyper* hyper, const Uses& use,
+           bool workspace_clean = false, bool static_scratch = false) {
     if (step == 0) return PACT_EINVAL;
     if (s.segs == nullptr && (hyper == nullptr || !hyper_ok(*hyper))) return PACT_EINVAL;
     uint64_t nslots = 0;
     int rc = validate(s, use, s.digest, &nslots);
     if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, hyper, step, true, &rc);
+    rc = check_segment_hypers(s);
     if (rc != PACT_OK) return rc;
+    if (static_scratch) {
+        if (s.workspace != nullptr) return PACT_EINVAL;
+        if (result_slots(s) > PACT_STATIC_MAX_SEGMENTS) return PACT_ESCRATCH;
+        void* lanes = nullptr;
+        rc = static_scratch_ptr(s.stream, &lanes);
+        if (rc != PACT_OK) return rc;
+        s.workspace = lanes;
+        s.workspace_bytes = kStaticScratchBytes;
+        workspace_clean = false;  // shared by every call on the GPU: always cleared first
+    }
+    const SegSource work{&s, hyper, step, true};
     return run(mode, s, work, s.digest, nslots, workspace_clean);
 }
 
@@ -412,8 +484,7 @@ int measure(pact::Mode mode, const View& s, const Uses& use, uint64_t* out) {
     uint64_t nslots = 0;
     int rc = validate(s, use, out, &nslots);
     if (rc != PACT_OK) return rc;
-    std::vector<SegWork> work = segment_work(s, nullptr, 0, false, &rc);
-    if (rc != PACT_OK) return rc;
+    const SegSource work{&s, nullptr, 0, false};
     return run(mode, s, work, out, nslots);
 }
 
@@ -450,6 +521,13 @@ int pact_adamw_commit_ex(const pact_shard* s, uint64_t step, const pact_hyper* h
 
 int pact_adamw_commit(const pact_shard* s, uint64_t step, const pact_hyper* hyper) {
     return pact_adamw_commit_ex(s, step, hyper, 0u);
+}
+
+int pact_adamw_commit_static(const pact_shard* s, uint64_t step, const pact_hyper* hyper, uint32_t flags) {
+    if (s == nullptr || (flags & ~PACT_COMMIT_ZERO_GRAD) != 0) return PACT_EINVAL;
+    const Uses use = {{true, true, true, true, true}};
+    const pact::Mode mode = (flags & PACT_COMMIT_ZERO_GRAD) ? pact::Mode::CommitZeroGrad : pact::Mode::Commit;
+    return commit(mode, view_of(s), step, hyper, use, false, true);
 }
 
 int pact_grad_guard(const pact_shard* s, uint64_t* dev_out) {
@@ -507,6 +585,7 @@ const char* pact_strerror(int code) {
         case PACT_EOVERLAP: return "buffers overlap";
         case PACT_ERANGE: return "index range reaches the digest tag bits (2^56), wraps, or exceeds one launch grid";
         case PACT_EHIP: return "HIP call failed";
+        case PACT_ESCRATCH: return "more segments than the library's static scratch holds";
         default: return "unknown error";
     }
 }

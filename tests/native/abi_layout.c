@@ -34,9 +34,9 @@ int main(void) {
     F(pact_shard_bf16, stream);
     CLOSE();
     printf(", \"codes\": {\"PACT_OK\": %d, \"PACT_EINVAL\": %d, \"PACT_EALIGN\": %d, \"PACT_EOVERLAP\": %d, "
-           "\"PACT_ERANGE\": %d, \"PACT_EHIP\": %d, \"PACT_COMMIT_ZERO_GRAD\": %u, "
-           "\"PACT_COMMIT_WORKSPACE_CLEAN\": %u}}\n",
-           PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP, PACT_COMMIT_ZERO_GRAD,
-           PACT_COMMIT_WORKSPACE_CLEAN);
+           "\"PACT_ERANGE\": %d, \"PACT_EHIP\": %d, \"PACT_ESCRATCH\": %d, \"PACT_COMMIT_ZERO_GRAD\": %u, "
+           "\"PACT_COMMIT_WORKSPACE_CLEAN\": %u, \"PACT_STATIC_MAX_SEGMENTS\": %d}}\n",
+           PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP, PACT_ESCRATCH,
+           PACT_COMMIT_ZERO_GRAD, PACT_COMMIT_WORKSPACE_CLEAN, PACT_STATIC_MAX_SEGMENTS);
     return 0;
 }

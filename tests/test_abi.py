@@ -29,8 +29,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_strerror_is_distinct_per_code():
-    texts = {code: pk._strerror(code) for code in (0, -1, -2, -3, -4, -5)}
-    assert len(set(texts.values())) == 6
+    texts = {code: pk._strerror(code) for code in (0, -1, -2, -3, -4, -5, -6)}
+    assert len(set(texts.values())) == 7
     assert pk._strerror(-99) == "unknown error"
 
 
