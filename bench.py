@@ -44,10 +44,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mistral7b_shard16")
-    ap.add_argument("--cpu-seconds", type=float, default=6.0,
-                    help="target seconds for each CPU oracle leg (single thread, all threads)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target seconds of the pinned single-thread CPU oracle leg (the multi-thread context "
+                         "leg takes half)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--no-parity", action="store_true", help="skip the in-run oracle replay of the timed commits")
+    ap.add_argument("--record-valu-ceiling", action="store_true",
+                    help="also write profiles/valu_ceiling_<kernel>.json from this run's cache-resident timings")
     ap.add_argument("--layout", choices=("spread", "packed"), default="spread",
                     help="spread: the five arrays in one ShardArena pool, each in its own region of HBM "
                          "(the library's recommended placement); packed: five separate allocations")
@@ -116,9 +120,10 @@ def record_traffic(workload: str, fetch_csv: str, write_csv: str) -> dict:
 
 def cpu_baseline(w, seconds: float) -> dict:
     """The oracle, unchanged, on a bounded sample: the first 2^24 elements of
-    the same shard.  Leg 1: one thread.  Leg 2: the sample cut into one slice
-    per host thread (the digest of the whole is the wrapping sum of the
-    slices).  Each leg repeats commits until `seconds` have passed."""
+    the same shard (same offset, distributions and step).  The reported
+    value: one thread pinned to one host core, repeating commit + digest
+    until `seconds` have passed.  Context: the same sample cut into one slice
+    per host thread (up to 16), run concurrently."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -131,11 +136,13 @@ def cpu_baseline(w, seconds: float) -> dict:
     b = np.zeros(n, np.uint16)
     h = oracle.Hyper(**(w.hypers[0]))
 
-    def leg(threads):
+    def leg(threads, budget, pin=None):
         cuts = [n * k // threads for k in range(threads + 1)]
 
         def one(args):
             k, step = args
+            if pin is not None:
+                os.sched_setaffinity(0, {pin})  # this thread only
             a, z = cuts[k], cuts[k + 1]
             return oracle.commit_and_digest(p[a:z], g[a:z], m[a:z], v[a:z], b[a:z], h, step, w.global_offset + a)
 
@@ -146,23 +153,69 @@ def cpu_baseline(w, seconds: float) -> dict:
                 done += n
                 step += 1
                 el = time.perf_counter() - t0
-                if el >= seconds:
+                if el >= budget:
                     return done / el
 
-    threads = max(1, min(16, os.cpu_count() or 1))
-    single = leg(1)
-    multi = leg(threads)
+    host_cpus = os.cpu_count() or 1
+    allowed = sorted(os.sched_getaffinity(0))
+    threads = max(1, min(16, len(allowed)))
+    single = leg(1, seconds, pin=allowed[0])
+    multi = leg(threads, seconds / 2)
     return {
-        "value": multi,
+        "value": single,
         "unit": "elements/s",
-        "cores": threads,
+        "cores": 1,
         "kind": "oracle",
-        "sample": f"first {n} elements of the {w.name} shard (same offset, distributions and step), "
-                  f"commit+digest repeated for >= {seconds:g} s per leg; the oracle cut into {threads} slices "
-                  f"run by {threads} threads",
-        "single_thread_value": single,
+        "sample": f"first {n} elements (at most 2^24) of the {w.name} shard (same offset, distributions and step), "
+                  f"commit+digest repeated for >= {seconds:g} s, one thread pinned to host core {allowed[0]}",
+        "budget_s": seconds,
+        "multi_thread": {"value": multi, "threads": threads,
+                         "note": f"the same sample cut into {threads} slices run by {threads} threads "
+                                 "(context, not the baseline)"},
+        "host_cpus": host_cpus,
         "cpu_model": _cpu_model(),
     }
+
+
+def oracle_replay(w, steps, want_digest: int, threads: int = 16, chunk: int = 1 << 24) -> dict:
+    """In-run parity: the oracle replays, on the host, the exact sequence of
+    commits the GPU ran (the generated state at the first step, the same
+    gradient for every commit, steps `steps`) over the whole shard, chunk by
+    chunk (each chunk cut into slices run by host threads; elements are
+    independent, so the digest is the wrapping sum), and its final digest
+    is compared with the GPU's."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import oracle
+    import workloads as wl
+
+    h = oracle.Hyper(**(w.hypers[0]))
+    threads = max(1, min(threads, len(os.sched_getaffinity(0))))
+    t0 = time.perf_counter()
+    total = 0
+
+    def replay(args):
+        p, g, m, v, b, first = args
+        for st in steps[:-1]:
+            oracle.adamw_commit(p, g, m, v, b, h, st)
+        return oracle.commit_and_digest(p, g, m, v, b, h, steps[-1], first)
+
+    import numpy as np
+
+    with ThreadPoolExecutor(threads) as ex:
+        for a in range(0, w.numel, chunk):
+            cnt = min(chunk, w.numel - a)
+            p, g, m, v = wl.arrays_host(w, a, cnt)
+            b = np.zeros(cnt, np.uint16)
+            cuts = [cnt * k // threads for k in range(threads + 1)]
+            jobs = [(p[x:y], g[x:y], m[x:y], v[x:y], b[x:y], w.global_offset + a + x)
+                    for x, y in zip(cuts[:-1], cuts[1:]) if y > x]
+            total += sum(ex.map(replay, jobs))
+    total &= (1 << 64) - 1
+    return {"checked": f"final digest after the {len(steps)} commits of steps {steps[0]}..{steps[-1]} "
+                       "(warm-up and timed), replayed by the oracle over the whole shard",
+            "oracle_digest": f"{total:#018x}", "gpu_digest": f"{want_digest:#018x}", "match": total == want_digest,
+            "seconds": time.perf_counter() - t0, "threads": threads}
 
 
 def _cpu_model() -> str:
@@ -360,6 +413,7 @@ def main():
           f"(min {main_m['min_launch_ms']:.4f}), {achieved:.1f} GB/s", file=sys.stderr, flush=True)
     last_digest = main_m["digest"]
     wall = main_m["wall_s"]
+    timed_steps = [w.first_step + args.warmup, w.first_step + args.warmup + K - 1]
 
     probe_res = None
     if not args.no_probe and segments is None:
@@ -382,6 +436,18 @@ def main():
             e_ev.record()
             torch.cuda.synchronize()
             return s_ev.elapsed_time(e_ev) / reps
+
+        def median_launch(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            ev[0].record()
+            for r in range(reps):
+                fn()
+                ev[r + 1].record()
+            torch.cuda.synchronize()
+            ts = sorted(ev[r].elapsed_time(ev[r + 1]) for r in range(reps))
+            return ts[reps // 2]
 
         reps = max(3, K // 2)
         zstep = [w.first_step + args.warmup + K]
@@ -417,11 +483,58 @@ def main():
                   "commit_bf16_state": "valu"}
         for name, fn, bpe in kernels:
             ms = time_call(fn, reps)
-            extra[name] = {"ms": ms, "bound": bounds[name], "bytes_per_element": bpe,
+            med = median_launch(fn, reps)
+            extra[name] = {"ms": ms, "median_launch_ms": med, "bound": bounds[name], "bytes_per_element": bpe,
                            "gbps": bpe * n / (ms / 1e3) / 1e9,
                            "frac_of_peak": bpe * n / (ms / 1e3) / 1e9 / PEAK_HBM_GBPS}
-            print(f"[bench] {name}: {ms:.4f} ms, {extra[name]['gbps']:.1f} GB/s at {bpe} B/element",
+            print(f"[bench] {name}: {ms:.4f} ms (median {med:.4f}), {extra[name]['gbps']:.1f} GB/s at {bpe} B/element",
                   file=sys.stderr, flush=True)
+
+        # VALU ceilings of the two VALU-heavy kernels: the same kernel on
+        # sub-shards small enough to stay in the 256 MB Infinity Cache, at two
+        # sizes; the slope of launch time over elements is the kernel's rate
+        # when HBM does not limit it (launch and tail costs cancel in the
+        # difference).  frac = the full-size time that rate allows / the
+        # measured full-size time.
+        def subshard_fn(name, m):
+            if name == "shard_digest":
+                ss = pk.Shard(tensors[0][:m], None, tensors[2][:m], tensors[3][:m], None,
+                              global_offset=w.global_offset)
+                return lambda: pk.shard_digest(ss)
+            ss = pk.ShardBf16(*(t[:m] for t in b16), global_offset=w.global_offset)
+            st = [w.first_step]
+
+            def f():
+                pk.adamw_commit_bf16(ss, st[0], hyper)
+                st[0] += 1
+            return f
+
+        for name, (n1, n2), bpe, ws in (("shard_digest", (1 << 22, 1 << 24), 12, 12),
+                                         ("commit_bf16_state", (1 << 22, 1 << 24), 14, 8)):
+            if name not in extra or n2 > n:
+                continue
+            t1 = median_launch(subshard_fn(name, n1), 40)
+            t2 = median_launch(subshard_fn(name, n2), 40)
+            rate = (n2 - n1) / ((t2 - t1) / 1e3)
+            full_ms = extra[name]["median_launch_ms"]
+            ceil = {"elements_per_s": rate, "full_size_ms_at_ceiling": n / rate * 1e3,
+                    "frac": (n / rate * 1e3) / full_ms,
+                    "bytes_per_s_at_ceiling": rate * bpe,
+                    "sizes": [n1, n2], "median_launch_ms": [t1, t2],
+                    "working_set_bytes": n2 * ws,
+                    "method": "slope of the median launch time between two cache-resident sub-shards "
+                              "(same kernel, same instruction mix); frac = full-size time at that rate / "
+                              "measured full-size median launch time"}
+            extra[name]["valu_ceiling"] = ceil
+            print(f"[bench] {name}: cache-resident rate {rate:.3e} elem/s -> {n / rate * 1e3:.4f} ms at full size, "
+                  f"frac {ceil['frac']:.3f} of that ceiling", file=sys.stderr, flush=True)
+            if args.record_valu_ceiling:
+                rec = dict(ceil, kernel=name, workload=w.name, full_size_elements=n, full_size_median_ms=full_ms,
+                           kernel_source_hash=kernel_source_hash(),
+                           command=f"python bench.py --workload {w.name} --record-valu-ceiling")
+                with open(os.path.join(ROOT, "profiles", f"valu_ceiling_{name}.json"), "w") as fh:
+                    json.dump(rec, fh, indent=1)
+                    fh.write("\n")
 
     other = None
     if not args.no_compare_layout:
@@ -434,7 +547,10 @@ def main():
             fill(o_t, o_b)
             o_sh = pk.Shard(*o_t, o_b, global_offset=w.global_offset, segments=segments, hypers=hypers)
             om = measure(o_sh, K, args.warmup)
-            other = {"layout": other_layout, "ms_per_step": om["ms_per_step"],
+            other = {"layout": other_layout,
+                     "note": ("five separate back-to-back allocations: the rate a caller that ignores the library's "
+                              "placement rule gets" if other_layout == "packed" else "the library's placement rule"),
+                     "ms_per_step": om["ms_per_step"],
                      "value": n / (om["ms_per_step"] / 1e3),
                      "achieved_gbps": algo_bytes / (om["avg_launch_ms"] / 1e3) / 1e9,
                      "frac": algo_bytes / (om["avg_launch_ms"] / 1e3) / 1e9 / PEAK_HBM_GBPS,
@@ -466,6 +582,19 @@ def main():
     for name, entry in extra.items():
         entry["valu"] = valu_of(name)
 
+    parity = None
+    all_steps = list(range(w.first_step, w.first_step + args.warmup + K))
+    if args.no_parity:
+        parity = {"skipped": "--no-parity"}
+    elif segments is not None or n * len(all_steps) > 2e10:
+        parity = {"skipped": "the in-run replay covers flat shards of up to 2e10 element-commits; "
+                             "this workload's parity is in the GPU tests"}
+    else:
+        print("[bench] oracle replay of the timed commits ...", file=sys.stderr, flush=True)
+        parity = oracle_replay(w, all_steps, last_digest)
+        print(f"[bench] parity: oracle {parity['oracle_digest']} gpu {parity['gpu_digest']} "
+              f"{'match' if parity['match'] else 'MISMATCH'} ({parity['seconds']:.1f} s)", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle baseline ...", file=sys.stderr, flush=True)
@@ -486,6 +615,9 @@ def main():
         "data": "synthetic (seeded Philox4x32-10 inputs with the workload's shapes and distributions)",
         "config": dict(w.describe(), parallelism="one rank's shard, no collectives",
                        bytes_per_element=BYTES_PER_ELEM,
+                       warmup_commits=args.warmup, timed_steps=timed_steps,
+                       state=(f"generated at step {w.first_step}, then evolved by every commit (warm-up commits at "
+                              f"steps {w.first_step}..{timed_steps[0] - 1}); the same gradient for every commit"),
                        layout=(f"spread: the five arrays in one ShardArena pool, {pk.ARENA_SPACING >> 30} GiB apart"
                                if args.layout == "spread" else "packed: five separate torch allocations")),
         "hbm_gbps_nominal": algo_bytes / (ms_per_step / 1e3) / 1e9,
@@ -510,6 +642,7 @@ def main():
                       "one-workgroup kernels that clear and sum the digest lanes (a few microseconds)",
         },
         "cpu_baseline": cpu,
+        "parity": parity,
         "probe": probe_res,
         "other_layout": other,
         "other_kernels": extra,

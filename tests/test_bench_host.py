@@ -91,3 +91,25 @@ def test_record_clock(sandbox):
     assert rec["kernels"]["probe"]["clock_ghz"] == pytest.approx(2.4)
     assert bench.stored_clock("mistral7b_shard16", "feedfacecafebeef")["kernels"]["commit"]["dispatches"] == 2
     assert bench.stored_clock("mistral7b_shard16", "0123456789abcdef") is None
+
+
+def test_oracle_replay_matches_a_direct_run_and_sees_a_wrong_digest():
+    """The in-run parity replay (chunked, threaded) equals the oracle run as
+    one plain sequence over the whole shard, and reports a mismatch."""
+    from dataclasses import replace
+
+    import numpy as np
+
+    import oracle
+
+    w = replace(wl.WORKLOADS["decoder1b_shard16"], numel=300_007)
+    p, g, m, v = wl.arrays_host(w)
+    b = np.zeros(w.numel, np.uint16)
+    h = oracle.Hyper(**w.hypers[0])
+    for st in (100, 101):
+        oracle.adamw_commit(p, g, m, v, b, h, st)
+    d = oracle.commit_and_digest(p, g, m, v, b, h, 102, w.global_offset)
+    r = bench.oracle_replay(w, [100, 101, 102], d, threads=3, chunk=100_000)
+    assert r["match"] and r["oracle_digest"] == f"{d:#018x}"
+    assert not bench.oracle_replay(w, [100, 101, 102], d ^ 1, threads=2, chunk=70_001)["match"]
+    assert not bench.oracle_replay(w, [100, 101], d, threads=2)["match"]
