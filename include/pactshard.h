@@ -237,6 +237,36 @@ int pact_shard_digest_bf16(const pact_shard_bf16* s);
 int64_t pact_digest_slots_bf16(const pact_shard_bf16* s);
 int64_t pact_workspace_bytes_bf16(const pact_shard_bf16* s);
 
+/* Placement of one shard's five arrays in one device pool.  On MI355X the
+ * commit's eight concurrent streams (reads of p, g, m, v; writes of p', m',
+ * v' and the bf16 copy) reach about 6.4-6.5 TB/s (80-81% of the 8 TB/s
+ * peak) when the arrays sit in separate regions of HBM some tens of GB
+ * apart, and about 5.6-5.7 TB/s (70-71%) when they sit within a few GB of
+ * each other -- the case of five back-to-back allocations.  The kernels are
+ * the same; the difference is the memory system's.  pact_arena_plan gives
+ * the library's placement rule as byte offsets into one pool the caller
+ * allocates (one hipMalloc of pool_bytes, 2 MiB aligned):
+ *   fp32 array k (0 param, 1 grad, 2 exp_avg, 3 exp_avg_sq) at k * spacing,
+ *   the bf16 copy at 4 * spacing, pool_bytes = 4 * spacing + its size;
+ * spacing = the requested one (at least one fp32 array, rounded up to
+ * 2 MiB), or with spacing == 0 the default: PACT_ARENA_SPACING when the
+ * five arrays together exceed PACT_ARENA_PACK_BELOW bytes, else the arrays
+ * back to back (a shard that small stays in the 256 MB on-chip cache and
+ * placement does not matter).  With the default spacing the pool reserves
+ * about 176 GiB for any shard above that size; the gaps after each fp32
+ * array (offset[k] + array bytes .. offset[k+1]) hold nothing of the shard
+ * and are free for the caller's other buffers.  Pure host arithmetic: no HIP
+ * call, no allocation.  PACT_EINVAL if out is NULL, PACT_ERANGE if the pool
+ * does not fit 64 bits. */
+#define PACT_ARENA_SPACING (44ull << 30)
+#define PACT_ARENA_PACK_BELOW (512ull << 20)
+typedef struct pact_arena_layout {
+    uint64_t pool_bytes;  /* bytes to allocate for the pool                        */
+    uint64_t spacing;     /* bytes between the starts of consecutive fp32 arrays    */
+    uint64_t offset[5];   /* byte offsets of param, grad, exp_avg, exp_avg_sq, bf16 */
+} pact_arena_layout;
+int pact_arena_plan(uint64_t numel, uint64_t spacing, pact_arena_layout* out);
+
 /* Measurement support, not part of the commit: streams the same bytes as a
  * commit (reads 4 fp32 arrays, writes 3 fp32 arrays and one 16-bit array,
  * 30 bytes per element) with no arithmetic beyond one add, so its rate is

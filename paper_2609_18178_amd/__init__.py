@@ -26,7 +26,7 @@ __all__ = [
     "Hyper", "Shard", "ShardBf16", "ShardArena", "PactError", "adamw_commit", "adamw_commit_static",
     "adamw_commit_bf16", "grad_guard",
     "shard_digest", "shard_digest_bf16", "bf16_digest", "stream_probe",
-    "digest_slots", "to_u64", "library_path",
+    "digest_slots", "to_u64", "library_path", "arena_plan",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -76,6 +76,10 @@ class _CShardBf16(ctypes.Structure):
     ]
 
 
+class _CArenaLayout(ctypes.Structure):
+    _fields_ = [("pool_bytes", ctypes.c_uint64), ("spacing", ctypes.c_uint64), ("offset", ctypes.c_uint64 * 5)]
+
+
 _LIB = None
 
 
@@ -114,6 +118,8 @@ def _lib():
         lib.pact_digest_slots.restype = ctypes.c_int64
         lib.pact_workspace_bytes.argtypes = [P]
         lib.pact_workspace_bytes.restype = ctypes.c_int64
+        lib.pact_arena_plan.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(_CArenaLayout)]
+        lib.pact_arena_plan.restype = ctypes.c_int
         lib.pact_stream_probe.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_uint64, ctypes.c_void_p]
         lib.pact_stream_probe.restype = ctypes.c_int
         lib.pact_strerror.argtypes = [ctypes.c_int]
@@ -283,13 +289,23 @@ class ShardBf16:
         return s
 
 
-# Default distance between the arrays of a ShardArena.
-ARENA_SPACING = 44 << 30
+# Default distance between the arrays of a ShardArena (the library's
+# PACT_ARENA_SPACING), and the size below which the arrays are packed.
+ARENA_SPACING = PACT_ARENA_SPACING = 44 << 30
+ARENA_PACK_BELOW = PACT_ARENA_PACK_BELOW = 512 << 20
+
+
+def arena_plan(numel: int, spacing: int = 0):
+    """The library's placement rule (``pact_arena_plan``): (pool bytes,
+    spacing, byte offsets of param, grad, exp_avg, exp_avg_sq, bf16)."""
+    out = _CArenaLayout()
+    _call("pact_arena_plan", _lib().pact_arena_plan(int(numel), int(spacing), ctypes.byref(out)))
+    return int(out.pool_bytes), int(out.spacing), [int(x) for x in out.offset]
 
 
 class ShardArena:
-    """Device memory for one shard's five arrays, each placed in its own
-    region of HBM.
+    """Device memory for one shard's five arrays, placed by the library's
+    rule (``pact_arena_plan``): each array in its own region of HBM.
 
     On MI355X the commit's eight concurrent streams (reads of p, g, m, v;
     writes of p', m', v' and the bf16 copy) move about 5.6 TB/s when all five
@@ -297,36 +313,30 @@ class ShardArena:
     when they are spread over four or five regions some tens of gigabytes
     apart (the same bytes, the same kernel; measured with the 30 B/element
     stream probe and with the commit itself).  The arena takes one device
-    pool and puts array k at byte offset k * spacing, so the arrays land far
-    apart in physical memory; the space between them stays usable through
+    pool and puts fp32 array k at byte offset k * spacing and the bf16 copy
+    at 4 * spacing; the space between the arrays stays usable through
     take().
 
-    spacing: bytes between array starts (default ARENA_SPACING = 44 GiB, at
-    least the largest array).  The pool holds 4 * spacing + the bf16 array.
+    spacing: bytes between array starts; 0 (default) takes the library's
+    rule: 44 GiB when the five arrays exceed 512 MiB, else back to back.
     Among even spacings of 24-60 GiB, 44, 56, 58 and 60 GiB measured about 1%
-    faster than 36-42, 48 and 52 GiB on two MI355X GPUs; 44 GiB is the smallest of
-    the fast ones.
+    faster than 36-42, 48 and 52 GiB on two MI355X GPUs; 44 GiB is the
+    smallest of the fast ones.
     """
 
     def __init__(self, numel: int, device=None, spacing: Optional[int] = None):
         device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
         if device.type != "cuda":
             raise TypeError("the arena lives on a GPU")
-        if spacing is None:
-            spacing = ARENA_SPACING
-        align = 2 << 20
-        f32 = (numel * 4 + align - 1) // align * align
-        b16 = (numel * 2 + align - 1) // align * align
-        self.spacing = max(int(spacing), f32)
-        self.spacing = (self.spacing + align - 1) // align * align
+        pool_bytes, self.spacing, offs = arena_plan(numel, spacing or 0)
         self.numel = numel
         self.device = device
-        self.pool = torch.empty(4 * self.spacing + b16, dtype=torch.uint8, device=device)
-        views = [self.pool[k * self.spacing: k * self.spacing + numel * 4].view(torch.float32) for k in range(4)]
+        self.pool = torch.empty(pool_bytes, dtype=torch.uint8, device=device)
+        views = [self.pool[offs[k]: offs[k] + numel * 4].view(torch.float32) for k in range(4)]
         self.param, self.grad, self.exp_avg, self.exp_avg_sq = views
-        self.param_bf16 = self.pool[4 * self.spacing: 4 * self.spacing + numel * 2].view(torch.int16)
+        self.param_bf16 = self.pool[offs[4]: offs[4] + numel * 2].view(torch.int16)
         # free gaps after each fp32 array: [start, end) in pool bytes
-        self._gaps = [[k * self.spacing + f32, (k + 1) * self.spacing] for k in range(4)]
+        self._gaps = [[offs[k] + numel * 4, offs[k + 1]] for k in range(4)]
 
     def take(self, nbytes: int, dtype=torch.uint8, region: Optional[int] = None) -> torch.Tensor:
         """A tensor carved from the space between the arrays (first fit, or

@@ -560,6 +560,22 @@ int pact_shard_digest_bf16(const pact_shard_bf16* s) {
     return measure(pact::Mode::DigestBf16State, view_of(s), use, s->digest_dev);
 }
 
+int pact_arena_plan(uint64_t numel, uint64_t spacing, pact_arena_layout* out) {
+    if (out == nullptr) return PACT_EINVAL;
+    constexpr uint64_t kAlign = 2ull << 20;
+    // every size below stays far from 2^64: numel < 2^56 keeps 4 * numel < 2^58
+    if (numel >= kIndexLimit || spacing > (1ull << 58)) return PACT_ERANGE;
+    auto round_up = [](uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; };
+    const uint64_t f32 = round_up(numel * 4), b16 = round_up(numel * 2);
+    uint64_t sp = spacing;
+    if (sp == 0) sp = (4 * f32 + b16 > PACT_ARENA_PACK_BELOW) ? PACT_ARENA_SPACING : f32;
+    sp = round_up(std::max(sp, f32));
+    out->spacing = sp;
+    for (int k = 0; k < 5; ++k) out->offset[k] = (uint64_t)k * sp;
+    out->pool_bytes = 4 * sp + b16;
+    return PACT_OK;
+}
+
 int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
                       float* out2, float* out3, uint16_t* out_half, uint64_t n, void* stream) {
     if (n == 0) return PACT_OK;

@@ -33,7 +33,12 @@ int main(void) {
     F(pact_shard_bf16, digest_dev); F(pact_shard_bf16, workspace); F(pact_shard_bf16, workspace_bytes);
     F(pact_shard_bf16, stream);
     CLOSE();
-    printf(", \"codes\": {\"PACT_OK\": %d, \"PACT_EINVAL\": %d, \"PACT_EALIGN\": %d, \"PACT_EOVERLAP\": %d, "
+    OPEN(pact_arena_layout);
+    F(pact_arena_layout, pool_bytes); F(pact_arena_layout, spacing); F(pact_arena_layout, offset);
+    CLOSE();
+    printf(", \"codes\": {\"PACT_ARENA_SPACING\": %llu, \"PACT_ARENA_PACK_BELOW\": %llu, ",
+           (unsigned long long)PACT_ARENA_SPACING, (unsigned long long)PACT_ARENA_PACK_BELOW);
+    printf("\"PACT_OK\": %d, \"PACT_EINVAL\": %d, \"PACT_EALIGN\": %d, \"PACT_EOVERLAP\": %d, "
            "\"PACT_ERANGE\": %d, \"PACT_EHIP\": %d, \"PACT_ESCRATCH\": %d, \"PACT_COMMIT_ZERO_GRAD\": %u, "
            "\"PACT_COMMIT_WORKSPACE_CLEAN\": %u, \"PACT_STATIC_MAX_SEGMENTS\": %d}}\n",
            PACT_OK, PACT_EINVAL, PACT_EALIGN, PACT_EOVERLAP, PACT_ERANGE, PACT_EHIP, PACT_ESCRATCH,

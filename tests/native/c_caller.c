@@ -85,18 +85,27 @@ int main(int argc, char** argv) {
     gen_fill(m, n, goff, seed, 2, 0, 0, 1e-4f / SUM_SD);
     gen_fill(v, n, goff, seed, 3, 0, 1, 1e-7f / SUM_SD);
 
-    /* device state, owned by this program */
+    /* device state, owned by this program: one pool, the five arrays placed
+     * by the library's rule */
     float *dp, *dg, *dm, *dv;
     uint16_t* db;
     uint64_t *dslot, *dbslot;
     void* ws;
+    char* pool;
     hipStream_t stream;
+    pact_arena_layout plan;
+    PACT_CHECK(pact_arena_plan(n, 0, &plan));
+    if (plan.offset[1] < n * 4 || plan.offset[4] + n * 2 > plan.pool_bytes || plan.offset[0] != 0) {
+        fprintf(stderr, "c_caller: placement plan does not hold the arrays\n");
+        return 2;
+    }
     HIP_CHECK(hipStreamCreate(&stream));
-    HIP_CHECK(hipMalloc((void**)&dp, n * 4));
-    HIP_CHECK(hipMalloc((void**)&dg, n * 4));
-    HIP_CHECK(hipMalloc((void**)&dm, n * 4));
-    HIP_CHECK(hipMalloc((void**)&dv, n * 4));
-    HIP_CHECK(hipMalloc((void**)&db, n * 2));
+    HIP_CHECK(hipMalloc((void**)&pool, plan.pool_bytes));
+    dp = (float*)(pool + plan.offset[0]);
+    dg = (float*)(pool + plan.offset[1]);
+    dm = (float*)(pool + plan.offset[2]);
+    dv = (float*)(pool + plan.offset[3]);
+    db = (uint16_t*)(pool + plan.offset[4]);
     HIP_CHECK(hipMalloc((void**)&dslot, 8));
     HIP_CHECK(hipMalloc((void**)&dbslot, 8));
     HIP_CHECK(hipMemcpy(dp, p, n * 4, hipMemcpyHostToDevice));
@@ -175,11 +184,7 @@ int main(int argc, char** argv) {
     HIP_CHECK(hipFree(ws));
     HIP_CHECK(hipFree(dbslot));
     HIP_CHECK(hipFree(dslot));
-    HIP_CHECK(hipFree(db));
-    HIP_CHECK(hipFree(dv));
-    HIP_CHECK(hipFree(dm));
-    HIP_CHECK(hipFree(dg));
-    HIP_CHECK(hipFree(dp));
+    HIP_CHECK(hipFree(pool));
     HIP_CHECK(hipStreamDestroy(stream));
     free(p);
     free(g);

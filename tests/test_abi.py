@@ -240,7 +240,7 @@ def test_header_is_c99_and_matches_the_binding(tmp_path):
                     "-o", str(exe), os.path.join(root, "tests", "native", "abi_layout.c")], check=True)
     c = json.loads(subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout)
     mirrors = {"pact_hyper": pk._CHyper, "pact_segment": pk._CSegment, "pact_shard": pk._CShard,
-               "pact_shard_bf16": pk._CShardBf16}
+               "pact_shard_bf16": pk._CShardBf16, "pact_arena_layout": pk._CArenaLayout}
     for name, cls in mirrors.items():
         assert ctypes.sizeof(cls) == c[name]["sizeof"], name
         py_fields = {f[0]: getattr(cls, f[0]).offset for f in cls._fields_}
@@ -387,3 +387,39 @@ def test_validation_fuzz():
         if digest_too:
             assert lib.pact_shard_digest(ctypes.byref(s)) == want, (case, violation)
         del keep
+
+
+# ---------------------------------------------------------------------------
+# the placement rule (pure host arithmetic)
+# ---------------------------------------------------------------------------
+MIB2 = 2 << 20
+
+
+@pytest.mark.parametrize("numel", [0, 1, 1000, 1 << 20, 10_000_001, 76_000_000, 453_001_472, 1_812_005_888,
+                                   7_248_023_552])
+def test_arena_plan_places_every_array_apart_and_in_the_pool(numel):
+    pool, spacing, off = pk.arena_plan(numel)
+    f32, b16 = numel * 4, numel * 2
+    assert spacing % MIB2 == 0 and all(o % MIB2 == 0 for o in off)
+    assert off == [k * spacing for k in range(5)]
+    assert spacing >= f32 and off[4] + b16 <= pool
+    total = 4 * ((f32 + MIB2 - 1) // MIB2 * MIB2) + (b16 + MIB2 - 1) // MIB2 * MIB2
+    if total > pk.PACT_ARENA_PACK_BELOW:
+        # the measured rule: arrays some tens of GB apart
+        assert spacing == max(pk.PACT_ARENA_SPACING, (f32 + MIB2 - 1) // MIB2 * MIB2)
+    else:
+        # small enough to stay in the on-chip cache: back to back
+        assert pool == total
+    assert pool < 288 * 10 ** 9  # fits one MI355X
+
+
+def test_arena_plan_explicit_spacing_and_errors():
+    pool, spacing, off = pk.arena_plan(1000, 3 << 20)
+    assert spacing == 4 << 20 and off[1] == 4 << 20
+    pool, spacing, off = pk.arena_plan(10 << 20, 1)  # never below one array
+    assert spacing == 40 << 20
+    lib = pk._lib()
+    assert lib.pact_arena_plan(10, 0, None) == pk.PACT_EINVAL
+    out = pk._CArenaLayout()
+    assert lib.pact_arena_plan(1 << 56, 0, ctypes.byref(out)) == pk.PACT_ERANGE
+    assert lib.pact_arena_plan(10, 1 << 59, ctypes.byref(out)) == pk.PACT_ERANGE
