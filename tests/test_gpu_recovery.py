@@ -61,3 +61,16 @@ def test_torn_commit_on_one_rank_is_rejected_at_agreement(tmp_path):
     assert all("torn" in r["why"] for r in first.results)
     assert out.ok and out.generation == 1
     _check(sv, out, 2)
+
+
+def test_ten_successive_repairs_keep_every_rank_bit_identical(tmp_path):
+    """Ten faults at committed boundaries over twelve updates (Sec. IV-G's
+    repeated-lifecycle check): ten in-memory repairs with no replay, and
+    every rank's final state equals the uninterrupted run's, bit for bit."""
+    faults = [{"rank": (3 * k) % 4, "site": "committed", "update": 2 + k} for k in range(10)]
+    sv, out = _run(tmp_path, 2, faults, updates=12, checkpoint_at=0)
+    assert out.ok and len(sv.cohorts) == 1, (out.exit_codes, sv.log_text(0, 0)[-3000:])
+    _check(sv, out, 2, updates=12)
+    for r in out.results:
+        assert r["generation"] == 10 and r["replayed_updates"] == 0 and len(r["repairs"]) == 10
+        assert {x["rebound_references"] for x in r["repairs"]} <= {0, 33}

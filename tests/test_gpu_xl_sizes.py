@@ -109,13 +109,14 @@ def test_mistral7b_whole_model_segments():
     print(f"[{w.name}] {counter['checked']} elements compared one by one", flush=True)
 
 
-def test_every_non_nan_pattern_through_the_commit():
-    """All 2^32 - 2^24 + 2 non-NaN binary32 patterns as weights, with lr = 0,
-    g = 0 and m = v = 0, so p' == p exactly (denormals, -0 and infinities
-    included) and the bf16 copy is the RNE of every pattern: compared through
-    the bf16 digest against the oracle's conversion, chunk by chunk.  (NaN
-    patterns are replaced by +0 on both sides; NaN payloads after arithmetic
-    are outside the contract.)"""
+def test_every_pattern_through_the_commit():
+    """All 2^32 binary32 patterns as weights, with lr = 0, g = 0 and
+    m = v = 0, so p' = p * 1 - 0: every non-NaN pattern comes back bit for
+    bit (denormals, -0 and infinities included) and every NaN stays a NaN.
+    The bf16 copy must be the RNE of the GPU's own p' (NaNs as the commit
+    left them, so the check does not depend on how the arithmetic treats NaN
+    payloads): compared through the bf16 digest against the oracle's
+    conversion of those bits, chunk by chunk."""
     from concurrent.futures import ThreadPoolExecutor
 
     import torch
@@ -129,22 +130,20 @@ def test_every_non_nan_pattern_through_the_commit():
     for start in range(0, 1 << 32, chunk):
         print(f"[all patterns] chunk at {start:#x}", flush=True)
         bits = torch.arange(start, start + chunk, dtype=torch.int64, device="cuda").to(torch.int32)
-        nan = (bits & 0x7FFFFFFF) > 0x7F800000
-        bits = torch.where(nan, torch.zeros_like(bits), bits)
+        p_before = bits.clone()
         p = bits.view(torch.float32)
-        del nan
         z = [torch.zeros(chunk, dtype=torch.float32, device="cuda") for _ in range(3)]
         b = torch.zeros(chunk, dtype=torch.int16, device="cuda")
         sh = pk.Shard(p, z[0], z[1], z[2], b, global_offset=start)
-        p_before = p.clone()
         pk.adamw_commit(sh, 1, hz)
-        assert torch.equal(p.view(torch.int32), p_before.view(torch.int32))
+        nan = (p_before & 0x7FFFFFFF) > 0x7F800000
+        assert torch.equal(p.view(torch.int32)[~nan], p_before[~nan])
+        assert bool(torch.isnan(p[nan]).all())
         assert not bool(z[1].view(torch.int32).any()) and not bool(z[2].view(torch.int32).any())
         got = pk.to_u64(pk.bf16_digest(sh))[0]
-        del p_before, z, sh, b, bits, p
+        hb = p.view(torch.int32).cpu().numpy().view(np.uint32)
+        del p_before, nan, z, sh, b, bits, p
         torch.cuda.empty_cache()
-        hb = np.arange(start, start + chunk, dtype=np.uint64).astype(np.uint32)
-        hb[(hb & 0x7FFFFFFF) > 0x7F800000] = 0
         cuts = [chunk * k // threads for k in range(threads + 1)]
 
         def part(k):
