@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--layout", choices=("spread", "packed"), default="spread",
                     help="spread: the five arrays in one ShardArena pool, each in its own region of HBM "
                          "(the library's recommended placement); packed: five separate allocations")
+    ap.add_argument("--spacing-gib", type=float, default=0.0,
+                    help="spread layout: GiB between the arrays (default 0: the library's placement rule)")
     ap.add_argument("--no-compare-layout", action="store_true",
                     help="skip timing the other layout as well")
     ap.add_argument("--record-clock", metavar="CLOCK_CSV",
@@ -248,12 +250,13 @@ def record_clock(workload: str, clock_csv: str) -> dict:
     import workloads as wl
 
     n = wl.WORKLOADS[workload].numel
+    full_grid = -(-n // 4096) * 256  # work-items of one full-shard launch (one 256-thread workgroup per tile)
     disp = {}
     with open(clock_csv) as f:
         for row in csv.DictReader(f):
             hit = [(key, bpe) for pat, key, bpe in CLOCK_KERNELS if pat in row["Kernel_Name"]]
-            if not hit:
-                continue
+            if not hit or int(row.get("Grid_Size", full_grid)) != full_grid:
+                continue  # other kernels, and the sub-shard launches of the VALU-ceiling timing
             d = disp.setdefault(int(row["Dispatch_Id"]), {"key": hit[0][0], "bpe": hit[0][1]})
             d[row["Counter_Name"]] = float(row["Counter_Value"])
             d["dur_s"] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) * 1e-9
@@ -336,7 +339,7 @@ def main():
 
     def allocate(layout):
         if layout == "spread":
-            arena = pk.ShardArena(n, dev)
+            arena = pk.ShardArena(n, dev, spacing=int(args.spacing_gib * (1 << 30)) or None)
             return arena, [arena.param, arena.grad, arena.exp_avg, arena.exp_avg_sq], arena.param_bf16
         ts = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(4)]
         return None, ts, torch.empty(n, dtype=torch.int16, device=dev)
@@ -541,7 +544,7 @@ def main():
         other_layout = "packed" if args.layout == "spread" else "spread"
         del sh
         free, _ = torch.cuda.mem_get_info(dev)
-        need = 4 * n * 4 + 2 * n if other_layout == "packed" else 4 * pk.ARENA_SPACING + 2 * n
+        need = 4 * n * 4 + 2 * n if other_layout == "packed" else pk.arena_plan(n, int(args.spacing_gib * (1 << 30)))[0]
         if free > need + (2 << 30):
             o_arena, o_t, o_b = allocate(other_layout)
             fill(o_t, o_b)
@@ -618,7 +621,8 @@ def main():
                        warmup_commits=args.warmup, timed_steps=timed_steps,
                        state=(f"generated at step {w.first_step}, then evolved by every commit (warm-up commits at "
                               f"steps {w.first_step}..{timed_steps[0] - 1}); the same gradient for every commit"),
-                       layout=(f"spread: the five arrays in one ShardArena pool, {pk.ARENA_SPACING >> 30} GiB apart"
+                       layout=(f"spread: the five arrays in one ShardArena pool, "
+                               f"{pk.arena_plan(n, int(args.spacing_gib * (1 << 30)))[1] / (1 << 30):g} GiB apart"
                                if args.layout == "spread" else "packed: five separate torch allocations")),
         "hbm_gbps_nominal": algo_bytes / (ms_per_step / 1e3) / 1e9,
         "pct_of_peak_hbm": 100.0 * algo_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,

@@ -144,9 +144,11 @@ __device__ __forceinline__ bool same_high_half(uint64_t first, uint64_t count) {
 // __builtin_sqrtf is lowered to the correctly rounded square root (the
 // -fhip-fp32-correctly-rounded-divide-sqrt default).  HIP's __fsqrt_rn is
 // NOT used: unless OCML_BASIC_ROUNDED_OPERATIONS is defined it maps to the
-// hardware's approximate v_sqrt_f32.
+// hardware's approximate v_sqrt_f32.  The update is split in two: the
+// moments, then the bias-corrected step, so that a tile can pick the form of
+// the square root once for all its elements (see sqrt_rn_in_range).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void adamw(float& p, float g, float& m, float& v, const StepScalars& s) {
+__device__ __forceinline__ void adamw_moments(float& p, float g, float& m, float& v, const StepScalars& s) {
     const float p_dec = p * s.decay;
     const float m_keep = s.beta1 * m;
     const float m_push = s.omb1 * g;
@@ -155,22 +157,84 @@ __device__ __forceinline__ void adamw(float& p, float g, float& m, float& v, con
     const float v_keep = s.beta2 * v;
     const float v_push = s.omb2 * g_sq;
     const float v_new = v_keep + v_push;
-    const float root = __builtin_sqrtf(v_new);
+    p = p_dec;
+    m = m_new;
+    v = v_new;
+}
+
+// Correctly rounded square root of x in [2^-96, +inf).  The hardware root
+// s = v_sqrt_f32(x) is within one ulp of sqrt(x) there (so is the compiler's
+// full sequence built on it), so the correctly rounded root is s or one of
+// its neighbours s_dn, s_up (bit patterns minus and plus one), and two exact
+// residuals decide which (the rounding test for square roots by fused
+// multiply-add, as in Markstein's and Goldschmidt-style refinements):
+//   x <= s_dn * s  => sqrt(x) lies below the midpoint of s_dn and s
+//                     (the geometric mean is below the arithmetic one);
+//   x >  s * s_up  => sqrt(x) lies above the midpoint of s and s_up: the
+//                     squared midpoint exceeds s * s_up by ulp^2 / 4, and
+//                     no binary32 x falls in that gap (x's grid near s^2 is
+//                     at least 2^22 of those units);
+//   otherwise s.
+// The residuals x - s_dn*s and x - s_up*s are computed by one FMA each; for
+// x >= 2^-96 they are multiples of 2^-142, so their signs come out exact
+// (denormals are kept).  The compiler's full sequence adds a rescaling of
+// inputs below 2^-96 and a class test for 0 and infinity; a tile whose
+// inputs all lie in [2^-96, +inf) takes this form (a wave-uniform branch),
+// any other tile the full one, with the same bits.
+__device__ __forceinline__ bool sqrt_rn_in_range(float x) {
+    return (__float_as_uint(x) - 0x0F800000u) < (0x7F800000u - 0x0F800000u);
+}
+
+__device__ __forceinline__ float sqrt_rn_in_range_root(float x) {
+    const float s = __builtin_amdgcn_sqrtf(x);
+    const float s_dn = __uint_as_float(__float_as_uint(s) - 1u);
+    const float s_up = __uint_as_float(__float_as_uint(s) + 1u);
+    const float r_dn = __builtin_fmaf(-s_dn, s, x);
+    const float r_up = __builtin_fmaf(-s_up, s, x);
+    const float t = r_dn <= 0.0f ? s_dn : s;
+    return r_up > 0.0f ? s_up : t;
+}
+
+template <bool InRange>
+__device__ __forceinline__ float adamw_step(float p_dec, float m_new, float v_new, const StepScalars& s) {
+    const float root = InRange ? sqrt_rn_in_range_root(v_new) : __builtin_sqrtf(v_new);
     const float den = root * s.rs_bc2 + s.eps;
     const float ratio = m_new / den;
     const float step = s.step_size * ratio;
-    p = p_dec - step;
-    m = m_new;
-    v = v_new;
+    return p_dec - step;
+}
+
+__device__ __forceinline__ void adamw(float& p, float g, float& m, float& v, const StepScalars& s) {
+    adamw_moments(p, g, m, v, s);
+    p = adamw_step<false>(p, m, v, s);
+}
+
+// The bias-corrected steps of all n elements of a lane's share of a tile
+// (p holds p*decay, m and v the new moments), with the short square root
+// when every v of the wave is in its range.
+template <int N>
+__device__ __forceinline__ void adamw_steps(float (&p)[N], const float (&m)[N], const float (&v)[N],
+                                            const StepScalars& s) {
+    bool in_range = true;
+#pragma unroll
+    for (int i = 0; i < N; ++i) in_range = in_range && sqrt_rn_in_range(v[i]);
+    if (__builtin_amdgcn_ballot_w64(!in_range) == 0) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) p[i] = adamw_step<true>(p[i], m[i], v[i], s);
+    } else {
+#pragma unroll
+        for (int i = 0; i < N; ++i) p[i] = adamw_step<false>(p[i], m[i], v[i], s);
+    }
 }
 
 // binary32 -> bfloat16, round to nearest even; NaN stays a quiet NaN with
 // its sign and top payload bits.  The rule, on the bits u of x:
 //   NaN:       (u >> 16) | 0x0040
 //   otherwise: (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-// gfx950's v_cvt_pk_bf16_f32 computes exactly this for every one of the 2^32
-// inputs (checked exhaustively on the device), two values per instruction,
-// so the kernels use it.
+// gfx950's v_cvt_pk_bf16_f32 computes exactly this, two values per
+// instruction, so the kernels use it: a GPU test sends all 2^32 patterns
+// through the commit as weights (p' = p * 1 - 0) and compares the bf16 copy
+// with this rule applied to the GPU's own p', NaNs included.
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
@@ -338,6 +402,9 @@ __device__ __forceinline__ uint64_t do_tile_vec(const Arrays& a, uint64_t e0, co
                 }
             }
             const auto rb = tile_rsrc(a.b + e0, kTile * 2);
+            // Bound by HBM: each row is updated and stored as soon as it is
+            // ready, with the full square root (the short in-range form of the
+            // BF16-state commit measured no faster here).
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 float p[4], m[4], v[4];
@@ -422,18 +489,32 @@ __device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0
         for (int r = 0; r < kRows; ++r) {
             G[r] = load16(rg, lane + r * kRowBytes);
         }
+        constexpr int kN = kRows * 8;
+        float p[kN], m[kN], v[kN];
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                float p0 = widen_lo(P[r][j]), p1 = widen_hi(P[r][j]);
-                float m0 = widen_lo(Mo[r][j]), m1 = widen_hi(Mo[r][j]);
-                float v0 = widen_lo(V[r][j]), v1 = widen_hi(V[r][j]);
-                adamw(p0, widen_lo(G[r][j]), m0, v0, sc);
-                adamw(p1, widen_hi(G[r][j]), m1, v1, sc);
-                P[r][j] = to_bf16x2(p0, p1);
-                Mo[r][j] = to_bf16x2(m0, m1);
-                V[r][j] = to_bf16x2(v0, v1);
+                const int i = r * 8 + 2 * j;
+                p[i] = widen_lo(P[r][j]);
+                p[i + 1] = widen_hi(P[r][j]);
+                m[i] = widen_lo(Mo[r][j]);
+                m[i + 1] = widen_hi(Mo[r][j]);
+                v[i] = widen_lo(V[r][j]);
+                v[i + 1] = widen_hi(V[r][j]);
+                adamw_moments(p[i], widen_lo(G[r][j]), m[i], v[i], sc);
+                adamw_moments(p[i + 1], widen_hi(G[r][j]), m[i + 1], v[i + 1], sc);
+            }
+        }
+        adamw_steps<kN>(p, m, v, sc);
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int i = r * 8 + 2 * j;
+                P[r][j] = to_bf16x2(p[i], p[i + 1]);
+                Mo[r][j] = to_bf16x2(m[i], m[i + 1]);
+                V[r][j] = to_bf16x2(v[i], v[i + 1]);
             }
             store16(P[r], rp, lane + r * kRowBytes);
             store16(Mo[r], rm, lane + r * kRowBytes);
@@ -505,11 +586,14 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
 // Waves per SIMD a kernel must be able to keep resident (caps its VGPRs).
 // The two standalone digests are bound by VALU issue and keep the full
 // eight waves per SIMD (the short index form would otherwise take the state
-// digest to 66 VGPRs and seven waves).  The BF16-state commit measured
-// fastest unbounded (88 VGPRs, five waves): capped at eight waves it spills,
-// at six or seven it is 0.5% slower.
+// digest to 66 VGPRs and seven waves).  The BF16-state commit, which holds
+// the moments of all its elements before the square roots, keeps five
+// (92 VGPRs; unbounded it takes 112 and four waves and measured 0.5% slower;
+// capped at six it spills).
 template <Mode M>
-constexpr unsigned kMinWavesPerSimd = (M == Mode::StateDigest || M == Mode::DigestBf16State) ? 8u : 1u;
+constexpr unsigned kMinWavesPerSimd = (M == Mode::StateDigest || M == Mode::DigestBf16State) ? 8u
+                                      : (M == Mode::CommitBf16State)                         ? 5u
+                                                                                             : 1u;
 
 template <Mode M>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kMinWavesPerSimd<M>)))

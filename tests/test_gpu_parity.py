@@ -858,3 +858,41 @@ def test_bf16_state_random_segment_tables(seed):
     assert pk.to_u64(pk.shard_digest_bf16(sh)) == want + [sum(want) & M64]
 
 
+
+
+def test_bf16_state_square_root_forms():
+    """The BF16-state commit takes a short exact square root in waves whose
+    second moments all lie in [2^-96, +inf) and the full one in any other
+    wave.  Waves planted on both sides of the boundary (v' = 2^-96 exactly,
+    one bf16 step below it, a denormal, zero, infinity; a whole tile of
+    zeros) and untouched waves: every output and the digest bit for bit
+    against the oracle."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    n = 16 * 4096
+    p, g, m, v = _bf16_arrays(w, 0, n)
+    plant = {  # element: (v bits, g bits) with beta2 = 0.5, so v' = v / 2 when g = 0
+        4 * 4096 + 5: (0x0000, 0x0000),          # v' = 0
+        5 * 4096 + 1000: (0x1000, 0x0000),       # v = 2^-95: v' = 2^-96, in range
+        6 * 4096 + 2000: (0x0FFF, 0x0000),       # v' one step below 2^-96
+        7 * 4096 + 3000: (0x0001, 0x0000),       # denormal v, v' denormal
+        8 * 4096 + 10: (0x7F80, 0x0000),         # v = +inf
+    }
+    for e, (vb, gb) in plant.items():
+        v[e], g[e] = vb, gb
+    v[9 * 4096:10 * 4096] = 0  # a whole tile of zero moments and gradients
+    g[9 * 4096:10 * 4096] = 0
+    m[9 * 4096:10 * 4096] = 0
+    for k in range(4):  # tile 10: one element out of range in each of its four waves
+        e = 10 * 4096 + k * 512 + 7
+        v[e], g[e] = 0x0001, 0x0000
+    h = dict(H, beta2=0.5)
+    t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (p, g, m, v)]
+    sh = pk.ShardBf16(*t, global_offset=w.global_offset)
+    got = pk.to_u64(pk.adamw_commit_bf16(sh, 3, g_hyper(h)))[0]
+    oracle.adamw_commit_bf16(p, g, m, v, o_hyper(h), 3)
+    for name, dev, ref in (("param", t[0], p), ("exp_avg", t[2], m), ("exp_avg_sq", t[3], v)):
+        assert_bitwise(name, host(dev).view(np.uint16), ref)
+    assert got == oracle.state_digest_bf16(p, m, v, w.global_offset)
