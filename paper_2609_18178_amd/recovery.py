@@ -137,6 +137,31 @@ class Envelope:
         return best if best is not None else Action.L2_RESTART
 
 
+# ---------------------------------------------------------------------------
+# break-even model of in-memory recovery (Sec. III-B, eq. (4))
+# ---------------------------------------------------------------------------
+
+def saving_per_recovery(age_updates: float, update_seconds: float, repair_seconds: float) -> float:
+    """S = A * t_update - T_repair: the replay of A = F - C updates that one
+    in-memory recovery avoids, less the repair itself (seconds)."""
+    return age_updates * update_seconds - repair_seconds
+
+
+def net_saving(n_eligible: float, saving: float, n_other: float, reject_cost: float, guard_overhead: float,
+               baseline_seconds: float) -> float:
+    """Delta T = N_eligible * S - N_other * C - h * T_0 (eq. (4)): the
+    cluster time a campaign of baseline length T_0 saves, with N_eligible
+    failures at committed boundaries, N_other uncommitted failures that each
+    cost C = T_detect + T_reject, and a boundary-guard overhead fraction h."""
+    return n_eligible * saving - n_other * reject_cost - guard_overhead * baseline_seconds
+
+
+def break_even_interval(saving: float, guard_overhead: float) -> float:
+    """Training time per eligible failure at which the savings pay for the
+    guard exactly (Delta T = 0 with no other failures): S / h seconds."""
+    return saving / guard_overhead
+
+
 class ModState(str, Enum):
     IDLE = "IDLE"
     FORWARD = "FORWARD"

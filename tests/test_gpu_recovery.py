@@ -74,3 +74,9 @@ def test_ten_successive_repairs_keep_every_rank_bit_identical(tmp_path):
     for r in out.results:
         assert r["generation"] == 10 and r["replayed_updates"] == 0 and len(r["repairs"]) == 10
         assert {x["rebound_references"] for x in r["repairs"]} <= {0, 33}
+    # repair-stage times, slowest rank per repair (as the paper reports them)
+    for phase in ("guard", "agree", "replace", "rebind", "release"):
+        per = [max(r["repairs"][k]["phases_ms"][phase] for r in out.results) for k in range(10)]
+        print(f"[gpu-recovery] {phase}: mean {sum(per) / 10:.3f} ms, min {min(per):.3f}, max {max(per):.3f}")
+    tot = [max(r["repairs"][k]["total_ms"] for r in out.results) for k in range(10)]
+    print(f"[gpu-recovery] guard to release: mean {sum(tot) / 10:.2f} ms, min {min(tot):.2f}, max {max(tot):.2f}")

@@ -217,3 +217,37 @@ def test_a_rank_of_an_old_generation_cannot_join(tmp_path):
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert time.monotonic() - t0 < 100
+
+
+def test_break_even_model_reproduces_the_papers_worked_example():
+    """Pin: eq. (4) of Sec. III-B evaluated on the paper's inputs gives the
+    figures it prints for them (tests/golden/break_even_example.txt), each to
+    the precision printed."""
+    g = {}
+    with open(os.path.join(ROOT, "tests", "golden", "break_even_example.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                k, v = line.split()
+                g[k] = float(v)
+    S = rc.saving_per_recovery(g["age_updates"], g["update_seconds"], g["repair_seconds"])
+    assert abs(S - g["saving_seconds"]) < 0.05
+    guard = g["guard_overhead"] * g["baseline_seconds"]
+    assert abs(guard - g["daily_guard_cost_seconds"]) < 0.05
+    days = rc.break_even_interval(S, g["guard_overhead"]) / 86400.0
+    assert abs(days - g["break_even_days"]) < 0.1
+    for pct, key in ((0.02, "2pct"), (0.10, "10pct")):
+        rate = pct * g["interruptions_per_day"]
+        assert abs(rate - g[f"eligible_per_day_at_{key}"]) < 0.0006
+    # the paper carries the event rates rounded to three decimals
+    rate2 = g["eligible_per_day_at_2pct"]
+    assert abs(1.0 / (0.02 * g["interruptions_per_day"]) - g["days_per_incident_at_2pct"]) < 0.01
+    assert abs(rate2 * S - g["daily_saving_at_2pct_seconds"]) < 0.1
+    assert abs(rate2 * S / guard - g["offset_fraction_at_2pct"]) < 0.001
+    rate10 = g["eligible_per_day_at_10pct"]
+    gross = rc.net_saving(rate10, S, 0, 0, 0, 0)
+    assert abs(gross - g["daily_gross_saving_at_10pct_seconds"]) < 0.15
+    net = rc.net_saving(rate10, S, 0, 0.1, g["guard_overhead"], g["baseline_seconds"])
+    assert abs(net - g["daily_net_saving_at_10pct_seconds"]) < 0.15
+    assert abs(net / guard - g["net_over_guard_cost_at_10pct"]) < 0.05
+    # rejections cost C each: C < 0.1 s (Sec. III-B) barely moves the balance
+    assert rc.net_saving(rate10, S, 5, 0.1, g["guard_overhead"], g["baseline_seconds"]) == pytest.approx(net - 0.5)
