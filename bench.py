@@ -59,6 +59,10 @@ def parse():
                     help="spread layout: GiB between the arrays (default 0: the library's placement rule)")
     ap.add_argument("--no-compare-layout", action="store_true",
                     help="skip timing the other layout as well")
+    ap.add_argument("--launch-shape", action="store_true",
+                    help="only compare launch shapes of the 30 B/element stream probe on the workload's arrays: one "
+                         "workgroup per tile against persistent grid-stride grids; writes "
+                         "profiles/launch_shape_<workload>.json")
     ap.add_argument("--record-clock", metavar="CLOCK_CSV",
                     help="write profiles/clock_<workload>.json (shader clock, VALU issue and VALU busy per kernel) "
                          "from a rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_INSTS_VALU SQ_ACTIVE_INST_VALU run of bench.py")
@@ -307,6 +311,63 @@ def stored_traffic(workload: str, src_hash: str):
     return rec
 
 
+def launch_shape(w, args) -> dict:
+    """The 30 B/element stream probe on the workload's arrays (spread layout,
+    zero-filled: the probe's cost does not depend on the values), launched
+    with one workgroup per tile (the kernels' shape) and from persistent
+    grids of 1-16 workgroups per CU striding over the tiles; median of 20
+    launches per shape, four rounds in alternating order, best round kept."""
+    import torch
+
+    import paper_2609_18178_amd as pk
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n = w.numel
+    arena = pk.ShardArena(n, dev, spacing=int(args.spacing_gib * (1 << 30)) or None)
+    ts = [arena.param, arena.grad, arena.exp_avg, arena.exp_avg_sq]
+    for t in ts:
+        t.zero_()
+    arena.param_bf16.zero_()
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    shapes = [0] + [cus * k for k in (1, 2, 4, 8, 16)]
+
+    def run(wg):
+        pk.stream_probe(ts[0], ts[1], ts[2], ts[3], ts[0], ts[2], ts[3], arena.param_bf16, workgroups=wg)
+
+    def median(wg, reps=20):
+        run(wg)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record()
+        for r in range(reps):
+            run(wg)
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        xs = sorted(ev[r].elapsed_time(ev[r + 1]) for r in range(reps))
+        return xs[reps // 2]
+
+    t_end = time.perf_counter() + PREWARM_S
+    while time.perf_counter() < t_end:
+        run(0)
+    torch.cuda.synchronize()
+    res = {wg: [] for wg in shapes}
+    for rnd in range(4):
+        for wg in (shapes if rnd % 2 == 0 else shapes[::-1]):
+            res[wg].append(median(wg))
+    best = {wg: min(v) for wg, v in res.items()}
+    out = {"workload": w.name, "elements": n, "cus": cus, "kernel_source_hash": kernel_source_hash(),
+           "command": f"python bench.py --workload {w.name} --launch-shape",
+           "shapes": [{"workgroups": ("one per tile" if wg == 0 else wg),
+                       "workgroups_per_cu": (None if wg == 0 else wg // cus),
+                       "median_ms": best[wg], "gbps": BYTES_PER_ELEM * n / (best[wg] / 1e3) / 1e9,
+                       "vs_one_per_tile": best[0] / best[wg]} for wg in shapes]}
+    with open(os.path.join(ROOT, "profiles", f"launch_shape_{w.name}.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    return out
+
+
 def main():
     args = parse()
     if args.record_clock:
@@ -326,6 +387,9 @@ def main():
     import workloads as wl
 
     w = wl.WORKLOADS[args.workload]
+    if args.launch_shape:
+        print(json.dumps(launch_shape(w, args)))
+        return
     if w.segments is not None:
         segments = list(w.segments)
         hypers = [pk.Hyper(**h) for h in w.hypers]

@@ -276,6 +276,14 @@ int pact_stream_probe(const float* in0, const float* in1, const float* in2, cons
                       float* out0, float* out2, float* out3, uint16_t* out_half,
                       uint64_t n, void* stream);
 
+/* The same probe from a persistent grid of `workgroups` workgroups of 256
+ * threads, each striding over the 4096-element tiles (workgroups == 0: one
+ * workgroup per tile, exactly pact_stream_probe).  Measurement support: it
+ * compares the grid-stride launch shape with the one the kernels use. */
+int pact_stream_probe_grid(const float* in0, const float* in1, const float* in2, const float* in3,
+                           float* out0, float* out2, float* out3, uint16_t* out_half,
+                           uint64_t n, uint32_t workgroups, void* stream);
+
 /* Static text for a PACT_E* code. */
 const char* pact_strerror(int code);
 

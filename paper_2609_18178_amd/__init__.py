@@ -122,6 +122,9 @@ def _lib():
         lib.pact_arena_plan.restype = ctypes.c_int
         lib.pact_stream_probe.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_uint64, ctypes.c_void_p]
         lib.pact_stream_probe.restype = ctypes.c_int
+        lib.pact_stream_probe_grid.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_uint64, ctypes.c_uint32,
+                                                                       ctypes.c_void_p]
+        lib.pact_stream_probe_grid.restype = ctypes.c_int
         lib.pact_strerror.argtypes = [ctypes.c_int]
         lib.pact_strerror.restype = ctypes.c_char_p
         lib.pact_last_hip_error.argtypes = []
@@ -481,11 +484,12 @@ def bf16_digest(shard: Shard, out: Optional[torch.Tensor] = None) -> torch.Tenso
     return out
 
 
-def stream_probe(i0, i1, i2, i3, o0, o2, o3, oh) -> None:
+def stream_probe(i0, i1, i2, i3, o0, o2, o3, oh, workgroups: int = 0) -> None:
     """30-byte/element streaming probe (measurement support): reads the four
     fp32 tensors i0..i3, writes o0, o2, o3 (fp32) and oh (16-bit); all on one
     GPU, contiguous, with the same element count.  Outputs may be the inputs
-    (in place)."""
+    (in place).  ``workgroups`` > 0: a persistent grid of that many
+    workgroups striding over the tiles instead of one workgroup per tile."""
     if not isinstance(i0, torch.Tensor):
         raise TypeError("i0 must be a torch tensor")
     n = i0.numel()
@@ -493,10 +497,10 @@ def stream_probe(i0, i1, i2, i3, o0, o2, o3, oh) -> None:
         _dev_tensor(t, (torch.float32,), name, n, i0.device)
     _dev_tensor(oh, (torch.int16, torch.bfloat16), "oh", n, i0.device)
     with torch.cuda.device(i0.device):
-        rc = _lib().pact_stream_probe(i0.data_ptr(), i1.data_ptr(), i2.data_ptr(), i3.data_ptr(),
-                                      o0.data_ptr(), o2.data_ptr(), o3.data_ptr(), oh.data_ptr(), n,
-                                      torch.cuda.current_stream(i0.device).cuda_stream)
-    _call("pact_stream_probe", rc)
+        rc = _lib().pact_stream_probe_grid(i0.data_ptr(), i1.data_ptr(), i2.data_ptr(), i3.data_ptr(),
+                                           o0.data_ptr(), o2.data_ptr(), o3.data_ptr(), oh.data_ptr(), n,
+                                           int(workgroups), torch.cuda.current_stream(i0.device).cuda_stream)
+    _call("pact_stream_probe_grid", rc)
 
 
 def to_u64(t: torch.Tensor):

@@ -655,16 +655,16 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(uint64_t* digest, uint64
 }
 
 // 30 bytes per element with no arithmetic beyond one add, through the same
-// instructions, tile shape and launch shape as the commit: the ceiling of the
-// commit's access pattern.  The outputs may alias the inputs element for
-// element (in place).  n is a multiple of 4; the last tile's resources end at
-// n, and a vector beyond it is dropped by the buffer range check.
-__global__ __launch_bounds__(kBlock) void probe_kernel(const float* i0, const float* i1, const float* i2,
-                                                       const float* i3, float* o0, float* o2, float* o3,
-                                                       uint16_t* oh, uint64_t n) {
+// instructions and tile shape as the commit: the ceiling of the commit's
+// access pattern.  The outputs may alias the inputs element for element (in
+// place).  n is a multiple of 4; the last tile's resources end at n, and a
+// vector beyond it is dropped by the buffer range check.
+__device__ __forceinline__ void probe_tile(const float* i0, const float* i1, const float* i2, const float* i3,
+                                           float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n,
+                                           uint64_t tile) {
     constexpr uint32_t kRow32 = kBlock * kVec * 4;
     constexpr uint32_t kRow16 = kBlock * kVec * 2;
-    const uint64_t e0 = (uint64_t)blockIdx.x * kTile;
+    const uint64_t e0 = tile * kTile;
     const uint64_t left = n - e0;
     const uint32_t cnt = left < (uint64_t)kTile ? (uint32_t)left : (uint32_t)kTile;
     const auto r0 = tile_rsrc(i0 + e0, cnt * 4), r1 = tile_rsrc(i1 + e0, cnt * 4);
@@ -694,6 +694,25 @@ __global__ __launch_bounds__(kBlock) void probe_kernel(const float* i0, const fl
         h.x = (s.x >> 16) | (s.y & 0xFFFF0000u);
         h.y = (s.z >> 16) | (s.w & 0xFFFF0000u);
         store8(h, wh, lane16 + u * kRow16);
+    }
+}
+
+// One workgroup per tile, as the commit launches.
+__global__ __launch_bounds__(kBlock) void probe_kernel(const float* i0, const float* i1, const float* i2,
+                                                       const float* i3, float* o0, float* o2, float* o3,
+                                                       uint16_t* oh, uint64_t n) {
+    probe_tile(i0, i1, i2, i3, o0, o2, o3, oh, n, blockIdx.x);
+}
+
+// The same work from a persistent grid: workgroup b takes tiles b, b + grid,
+// b + 2 grid, ... (the grid-stride shape), for comparison with one
+// workgroup per tile.
+__global__ __launch_bounds__(kBlock) void probe_persistent_kernel(const float* i0, const float* i1,
+                                                                  const float* i2, const float* i3, float* o0,
+                                                                  float* o2, float* o3, uint16_t* oh, uint64_t n) {
+    const uint64_t tiles = (n + kTile - 1) / kTile;
+    for (uint64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+        probe_tile(i0, i1, i2, i3, o0, o2, o3, oh, n, t);
     }
 }
 
@@ -747,10 +766,16 @@ hipError_t launch_finish(uint64_t* digest, uint64_t* lanes, uint32_t nres, bool 
 }
 
 hipError_t launch_probe(const float* i0, const float* i1, const float* i2, const float* i3,
-                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, hipStream_t stream) {
-    const uint64_t tiles = (n + kTile - 1) / kTile;
-    hipLaunchKernelGGL(probe_kernel, dim3((uint32_t)tiles), dim3(kBlock), 0, stream, i0, i1, i2, i3, o0, o2, o3,
-                       oh, n);
+                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, uint32_t workgroups,
+                        hipStream_t stream) {
+    if (workgroups == 0) {
+        const uint64_t tiles = (n + kTile - 1) / kTile;
+        hipLaunchKernelGGL(probe_kernel, dim3((uint32_t)tiles), dim3(kBlock), 0, stream, i0, i1, i2, i3, o0, o2,
+                           o3, oh, n);
+    } else {
+        hipLaunchKernelGGL(probe_persistent_kernel, dim3(workgroups), dim3(kBlock), 0, stream, i0, i1, i2, i3, o0,
+                           o2, o3, oh, n);
+    }
     return hipGetLastError();
 }
 

@@ -90,8 +90,11 @@ hipError_t launch_batch_bf16(Mode mode, const ArraysBf16& a, const Batch& b, uin
 // given) for r < nres, and, with per-segment results, digest[nres] = their sum.
 hipError_t launch_finish(uint64_t* digest, uint64_t* lanes, uint32_t nres, bool per_segment, hipStream_t stream);
 
-// Enqueue the 30-byte/element stream probe (n a multiple of kVec).
+// Enqueue the 30-byte/element stream probe (n a multiple of kVec): one
+// workgroup per tile when workgroups == 0, else a persistent grid of that
+// many workgroups striding over the tiles.
 hipError_t launch_probe(const float* i0, const float* i1, const float* i2, const float* i3,
-                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, hipStream_t stream);
+                        float* o0, float* o2, float* o3, uint16_t* oh, uint64_t n, uint32_t workgroups,
+                        hipStream_t stream);
 
 }  // namespace pact

@@ -576,8 +576,9 @@ int pact_arena_plan(uint64_t numel, uint64_t spacing, pact_arena_layout* out) {
     return PACT_OK;
 }
 
-int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
-                      float* out2, float* out3, uint16_t* out_half, uint64_t n, void* stream) {
+int pact_stream_probe_grid(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
+                           float* out2, float* out3, uint16_t* out_half, uint64_t n, uint32_t workgroups,
+                           void* stream) {
     if (n == 0) return PACT_OK;
     if (!in0 || !in1 || !in2 || !in3 || !out0 || !out2 || !out3 || !out_half || (n % pact::kVec) != 0) {
         return PACT_EINVAL;
@@ -586,11 +587,17 @@ int pact_stream_probe(const float* in0, const float* in1, const float* in2, cons
         !aligned(out2, 16) || !aligned(out3, 16) || !aligned(out_half, 8)) {
         return PACT_EALIGN;
     }
-    if ((n + pact::kTile - 1) / pact::kTile > (uint64_t)(UINT32_MAX / pact::kBlock)) return PACT_ERANGE;
-    hipError_t e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n,
+    const uint64_t tiles = (n + pact::kTile - 1) / pact::kTile;
+    if (tiles > (uint64_t)(UINT32_MAX / pact::kBlock) || workgroups > UINT32_MAX / pact::kBlock) return PACT_ERANGE;
+    hipError_t e = pact::launch_probe(in0, in1, in2, in3, out0, out2, out3, out_half, n, workgroups,
                                       static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail_hip(e);
     return PACT_OK;
+}
+
+int pact_stream_probe(const float* in0, const float* in1, const float* in2, const float* in3, float* out0,
+                      float* out2, float* out3, uint16_t* out_half, uint64_t n, void* stream) {
+    return pact_stream_probe_grid(in0, in1, in2, in3, out0, out2, out3, out_half, n, 0u, stream);
 }
 
 const char* pact_strerror(int code) {
