@@ -530,8 +530,12 @@ def main():
         if segments is None:
             b16 = []
             for k, t in enumerate(tensors):
-                dst = (arena.take(n * 2, torch.int16, region=k) if arena is not None
-                       else torch.empty(n, dtype=torch.int16, device=dev))
+                try:  # in the gap after fp32 array k when the arena spreads the arrays
+                    dst = arena.take(n * 2, torch.int16, region=k) if arena is not None else None
+                except MemoryError:  # a packed arena (small shard) has no gaps
+                    dst = None
+                if dst is None:
+                    dst = torch.empty(n, dtype=torch.int16, device=dev)
                 dst.view(torch.bfloat16).copy_(t)
                 b16.append(dst)
             sh16 = pk.ShardBf16(*b16, global_offset=w.global_offset)
