@@ -154,3 +154,34 @@ def test_static_commit_argument_errors_leave_state_untouched():
     b = pk.to_u64(pk.adamw_commit_static(sta2, 3))
     assert a == b and len(b) == pk.PACT_STATIC_MAX_SEGMENTS + 1
     assert b[-1] == sum(b[:-1]) & M64
+
+
+def test_static_commit_replays_from_a_hip_graph():
+    """The use the allocation-free commit is for: captured into a HIP graph
+    (the scratch is cleared by a kernel inside the graph, not a memset) and
+    replayed three times with eager work in between, each replay equal to
+    one more eager commit at the captured step, digests and state bit for
+    bit.  An eager call on the device comes first (it looks up the scratch
+    address)."""
+    import torch
+
+    pk = _pk()
+    segs, n, hyp = _table(21, 12, 9000)
+    eager, graphed, _ = _pair(n, 1 << 33, segs, hyp)
+    want = [pk.to_u64(pk.adamw_commit_static(eager, 9)) for _ in range(3)]
+    p_before = host(graphed.param).copy()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            pk.adamw_commit_static(graphed, 9)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert_bitwise("param before replay", host(graphed.param), p_before)
+    for k in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        assert pk.to_u64(graphed.digest) == want[k], k
+        _ = (torch.ones(1024, device="cuda") * 2).sum().item()  # unrelated eager work in between
+    _same(eager, graphed, "after three replays")
