@@ -449,6 +449,8 @@ class CohortSpec:
     resource: str = "hsdp"
     objective: str = "continue"
     envelope: Optional[Dict[str, str]] = None  # "platform|resource|phase|objective" -> "L1" / "L2"
+    generation_index: int = 0   # which cohort of the job this is (data-plane faults name the cohort they hit)
+    replay_to: int = 0          # frontier the failed cohort reached (a restart replays up to it)
 
 
 class Rank:
@@ -459,6 +461,8 @@ class Rank:
         self.result = {"rank": rank, "shard": self.shard_idx, "generation": spec.generation, "repairs": [],
                        "replayed_updates": 0, "exit": None}
         self.repairs = 0
+        self.generation = spec.generation
+        self.frontier = 0
         self.watch = Watchdog(self.log)
         entries = None
         if spec.envelope is not None:
@@ -468,8 +472,7 @@ class Rank:
 
     # -- plumbing ----------------------------------------------------------
     def log(self, msg: str):
-        print(f"[rank {self.rank} g{self.generation if hasattr(self, 'generation') else '?'}] {msg}",
-              file=sys.stderr, flush=True)
+        print(f"[rank {self.rank} g{self.generation}] {msg}", file=sys.stderr, flush=True)
 
     def write_result(self):
         path = os.path.join(self.spec.workdir, f"rank{self.rank}_g{self.spec.generation}.json")
@@ -480,8 +483,8 @@ class Rank:
     def end(self, code: int, why: str):
         self.result["exit"] = code
         self.result["why"] = why
-        self.result["frontier"] = getattr(self, "frontier", 0)
-        self.result["generation"] = getattr(self, "generation", self.spec.generation)
+        self.result["frontier"] = self.frontier
+        self.result["generation"] = self.generation
         self.log(f"exit {EXIT_NAMES.get(code, code)}: {why}")
         try:
             self.write_result()
@@ -532,8 +535,6 @@ class Rank:
         cls = load_engine(sp.engine)
         args = dict(sp.engine_args)
         self.engine = cls(numel=sp.numel, global_offset=self.shard_idx * sp.numel, seed=sp.seed, **args)
-        self.generation = sp.generation
-        self.frontier = 0
         self.committed_digest = 0
 
     # -- the data plane --------------------------------------------------------
@@ -776,12 +777,7 @@ def rank_main(argv=None) -> None:
     ap.add_argument("--rank", type=int, required=True)
     a = ap.parse_args(argv)
     with open(a.spec) as f:
-        d = json.load(f)
-    gi = d.pop("generation_index", 0)
-    replay_to = d.pop("replay_to", 0)
-    spec = CohortSpec(**d)
-    spec.generation_index = gi
-    spec.replay_to = replay_to
+        spec = CohortSpec(**json.load(f))
     r = Rank(spec, a.rank)
     try:
         r.watch.arm("setup", spec.control_timeout + 30.0)
