@@ -106,29 +106,84 @@ struct IndexAny {
 // IndexHi32: for a tile whose indices all share their upper 32 bits `hi`
 // (every tile but one that crosses a multiple of 2^32).  With index = hi:lo
 // the word only meets the low half, so
-//   (word ^ index) + gamma_k = zext(word ^ lo) + ((hi << 32) + gamma_k)
-// where gamma_k = gamma + (k << 56) is the tagged constant above.  The right
-// term is one wave-uniform 64-bit value per tag, kept in scalar registers,
-// and the sum is one v_mad_u64_u32 (word ^ lo) * 1 + G_k: no 64-bit index
-// arithmetic and no register pair to assemble for each word.
+//   z = (word ^ index) + gamma_k = zext(x) + G_k,   x = word ^ lo,
+// where gamma_k = gamma + (k << 56) is the tagged constant above and
+// G_k = (hi << 32) + gamma_k is one wave-uniform 64-bit value per tag.  Its
+// low half is gamma's (the same for every tile and tag), so z's halves are
+//   z_lo = x + G_lo (carry c),   z_hi = G_hi + c,
+// and z_hi takes one of two values.  The first mixing round then reads the
+// carry instead of a 64-bit value:
+//   z ^ (z >> 30):  lo1 = z_lo ^ alignbit(z_hi, z_lo, 30),
+//                   hi1 = z_hi ^ (z_hi >> 30), one of H_0, H_1 (c = 0, 1);
+//   times C1 = CHI:CLO, low 64 bits: lo1 * CLO + ((lo1 * CHI + hi1 * CLO) << 32),
+// and hi1 * CLO is one of K_0, K_1 = H_c * CLO mod 2^32.  So the product is
+//   prod  = lo1 * CLO + (K_0 << 32)          v_mad_u64_u32, scalar addend
+//   cross = lo1 * CHI + (c ? K_1 - K_0 : 0)  v_mad_u64_u32, low half used
+//   z1    = prod + (cross << 32)             v_add_u32 on the high half
+// with the carry, z_hi and the select taken by three VOP2 instructions that
+// share the carry in VCC.  Against the plain round this trades a 64-bit
+// shift, a multiply and the 64-bit index add (five VOP3 instructions) for
+// three VOP3 and two more VOP2 ones; the later rounds are unchanged.
 struct IndexHi32 {
-    uint32_t lo;   // low half of the lane's first index
-    uint64_t g[4]; // (hi << 32) + gamma + (tag << 56) for tags 0..3
+    static constexpr uint32_t kGammaLo = (uint32_t)kGamma;
+    uint32_t lo;        // low half of the lane's first index
+    uint32_t ghi[4];    // G_hi per tag
+    uint32_t kdiff[4];  // K_1 - K_0 per tag
+    uint64_t k0hi[4];   // K_0 << 32 per tag
     __device__ __forceinline__ IndexHi32(uint64_t tile_first, uint32_t lane_off)
         : lo((uint32_t)tile_first + lane_off) {
+        constexpr uint32_t clo = (uint32_t)kMul1;
         const uint64_t high = tile_first & 0xFFFFFFFF00000000ull;
 #pragma unroll
         for (uint32_t k = 0; k < 4; ++k) {
-            g[k] = high + kGamma + ((uint64_t)k << 56);
+            const uint32_t h = (uint32_t)((high + kGamma + ((uint64_t)k << 56)) >> 32);
+            const uint32_t h1 = h + 1u;
+            const uint32_t k0 = (h ^ (h >> 30)) * clo;
+            const uint32_t k1 = (h1 ^ (h1 >> 30)) * clo;
+            ghi[k] = h;
+            kdiff[k] = k1 - k0;
+            k0hi[k] = (uint64_t)k0 << 32;
         }
     }
     template <uint32_t Tag>
     __device__ __forceinline__ uint64_t hash(uint32_t word, uint32_t off) const {
         static_assert(Tag < 4, "array tags 0..3");
+        constexpr uint32_t clo = (uint32_t)kMul1, chi = (uint32_t)(kMul1 >> 32);
         const uint32_t x = word ^ (lo + off);
-        uint64_t z, carry;
-        asm("v_mad_u64_u32 %0, %1, %2, 1, %3" : "=v"(z), "=s"(carry) : "v"(x), "s"(g[Tag]));
-        return splitmix_mix(z);
+        uint32_t zlo, zhi, ksel;
+        // VCC carries c from the add to the select and to z_hi; a VALU write
+        // of VCC needs two wait states before a VALU reads it as a lane mask.
+        asm("v_add_co_u32_e32 %0, vcc, %3, %4\n\t"
+            "s_nop 1\n\t"
+            "v_cndmask_b32_e32 %1, 0, %5, vcc\n\t"
+            "v_addc_co_u32_e32 %2, vcc, 0, %6, vcc"
+            : "=&v"(zlo), "=&v"(ksel), "=v"(zhi)
+            : "s"(kGammaLo), "v"(x), "v"(kdiff[Tag]), "v"(ghi[Tag])
+            : "vcc");
+        const uint32_t lo1 = zlo ^ __builtin_amdgcn_alignbit(zhi, zlo, 30);
+        uint64_t prod, cross, carry0, carry1;
+        asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(prod), "=s"(carry0) : "v"(lo1), "v"(clo), "s"(k0hi[Tag]));
+        // Only cross's low half is used, so the addend's high half may hold
+        // anything: z_hi, which sits beside the select in the register pair.
+        asm("v_mad_u64_u32 %0, %1, %2, %3, %4"
+            : "=v"(cross), "=s"(carry1)
+            : "v"(lo1), "s"(chi), "v"(((uint64_t)zhi << 32) | ksel));
+        uint32_t res_hi;
+        asm("v_add_u32_e32 %0, %1, %2" : "=v"(res_hi) : "v"((uint32_t)(prod >> 32)), "v"((uint32_t)cross));
+        uint64_t z = ((uint64_t)res_hi << 32) | (uint32_t)prod;
+        z = z ^ (z >> 27);
+        {
+            constexpr uint32_t c2lo = (uint32_t)kMul2, c2hi = (uint32_t)(kMul2 >> 32);
+            const uint32_t zl = (uint32_t)z, zh = (uint32_t)(z >> 32);
+            const uint32_t t = zl * c2hi;
+            uint64_t cr, pr, cy0, cy1;
+            asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cr), "=s"(cy0) : "v"(zh), "s"(c2lo), "v"(((uint64_t)zh << 32) | t));
+            asm("v_mad_u64_u32 %0, %1, %2, %3, 0" : "=v"(pr), "=s"(cy1) : "v"(zl), "s"(c2lo));
+            uint32_t rh;
+            asm("v_add_u32_e32 %0, %1, %2" : "=v"(rh) : "v"((uint32_t)(pr >> 32)), "v"((uint32_t)cr));
+            z = ((uint64_t)rh << 32) | (uint32_t)pr;
+        }
+        return z ^ (z >> 31);
     }
 };
 
