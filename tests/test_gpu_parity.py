@@ -860,6 +860,58 @@ def test_bf16_state_random_segment_tables(seed):
 
 
 
+def test_bf16_state_edge_operands():
+    """Operands of the bias-corrected step at the edges of what training
+    produces, through the BF16-state commit.  With beta1 = beta2 = 1/2 and
+    g = 0 a planted m or v gives m' = m / 2 and v' = v / 2 exactly: m' =
+    2^-63, one bf16 step below it, -2^-63, just below 2, 2, -0 and 0 (one in
+    each wave of a tile), v' just below 2^64 and 2^64.  Then eps at 2^-57,
+    2^-56, 2^44 and 2^45 (the denominator from the root alone, and from eps
+    alone), and beta2 = 1 - 2^-24 at step 1, where rs_bc2 = 2^12, its largest value.
+    Every output and the digest bit for bit against the oracle."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    n = 16 * 4096
+    p0, g0, m0, v0 = _bf16_arrays(w, 0, n)
+
+    def run(p, g, m, v, h, step):
+        t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (p, g, m, v)]
+        sh = pk.ShardBf16(*t, global_offset=w.global_offset)
+        got = pk.to_u64(pk.adamw_commit_bf16(sh, step, g_hyper(h)))[0]
+        oracle.adamw_commit_bf16(p, g, m, v, o_hyper(h), step)
+        for name, dev, ref in (("param", t[0], p), ("exp_avg", t[2], m), ("exp_avg_sq", t[3], v)):
+            assert_bitwise(name, host(dev).view(np.uint16), ref)
+        assert got == oracle.state_digest_bf16(p, m, v, w.global_offset)
+
+    p, g, m, v = (a.copy() for a in (p0, g0, m0, v0))
+    plant_m = {  # tile: m bits (m' = m / 2)
+        4: 0x2080,   # m' = 2^-63, in range
+        5: 0x207F,   # m' one step below 2^-63
+        6: 0xA080,   # m' = -2^-63
+        7: 0x407F,   # m' just below 2
+        8: 0x4080,   # m' = 2
+        9: 0x8000,   # m' = -0
+    }
+    for tile, mb in plant_m.items():
+        e = tile * 4096 + 1234
+        m[e], g[e] = mb, 0
+    for tile, vb in ((10, 0x5FFF), (11, 0x6000)):  # v' just below 2^64, and 2^64
+        e = tile * 4096 + 77
+        v[e], g[e] = vb, 0
+    for k in range(4):  # tile 12: m' = 0 in each of its four waves
+        e = 12 * 4096 + k * 512 + 9
+        m[e], g[e] = 0, 0
+    run(p, g, m, v, dict(H, beta1=0.5, beta2=0.5), 3)
+    for eps in (2.0 ** -57, 2.0 ** -56, 2.0 ** 44, 2.0 ** 45):
+        p, g, m, v = (a.copy() for a in (p0, g0, m0, v0))
+        run(p, g, m, v, dict(H, eps=eps), 3)
+    p, g, m, v = (a.copy() for a in (p0, g0, m0, v0))
+    run(p, g, m, v, dict(H, beta2=float(np.float32(1.0) - np.float32(2.0 ** -24))), 1)
+    del torch
+
+
 def test_bf16_state_square_root_forms():
     """The BF16-state commit takes a short exact square root in waves whose
     second moments all lie in [2^-96, +inf) and the full one in any other
