@@ -13,10 +13,11 @@
 // ragged tail or a misaligned segment goes element by element.
 //
 // The digest is accumulated per thread in a 64-bit register (wrapping add),
-// reduced across the wave with shuffles and across the workgroup's four
-// waves through LDS, and added with one 64-bit atomic per workgroup into one
-// of kLanes workspace words of its result slot (256 bytes apart, so the
-// atomics of neighbouring workgroups do not queue on one address); a final
+// summed over the workgroup with 64-bit LDS atomics (one word per wave, the
+// four words added by thread 0), and added with one 64-bit atomic per
+// workgroup into one of kLanes workspace words of its result slot (256 bytes
+// apart, so the atomics of neighbouring workgroups do not queue on one
+// address); a final
 // one-workgroup kernel sums the lanes and sets them back to zero, so a call
 // that is told its workspace is clear can skip clearing it.  Without a
 // workspace the atomics go to the result slot itself.  Wrapping addition is
@@ -28,6 +29,7 @@
 // unit is built with -ffp-contract=off and without fast-math), correctly
 // rounded sqrt and division, fp32 denormals kept.
 #include "launch.h"
+
 
 // No fused multiply-add anywhere in this file, whatever the command line says.
 #pragma clang fp contract(off)
@@ -138,8 +140,14 @@ struct IndexHi32 {
         for (uint32_t k = 0; k < 4; ++k) {
             const uint32_t h = (uint32_t)((high + kGamma + ((uint64_t)k << 56)) >> 32);
             const uint32_t h1 = h + 1u;
-            const uint32_t k0 = (h ^ (h >> 30)) * clo;
-            const uint32_t k1 = (h1 ^ (h1 >> 30)) * clo;
+            // Wave-uniform per tile: computed on the scalar unit (left to
+            // itself the compiler forms them with VALU instructions, because
+            // their uses below want VGPRs), then copied once into VGPRs.
+            uint32_t k0, k1;
+            asm("s_lshr_b32 %0, %1, 30\n\ts_xor_b32 %0, %0, %1\n\ts_mul_i32 %0, %0, %2"
+                : "=&s"(k0) : "s"(h), "s"(clo) : "scc");
+            asm("s_lshr_b32 %0, %1, 30\n\ts_xor_b32 %0, %0, %1\n\ts_mul_i32 %0, %0, %2"
+                : "=&s"(k1) : "s"(h1), "s"(clo) : "scc");
             ghi[k] = h;
             kdiff[k] = k1 - k0;
             k0hi[k] = (uint64_t)k0 << 32;
@@ -593,7 +601,7 @@ __device__ __forceinline__ uint64_t do_tile_vec(const ArraysBf16& a, uint64_t e0
 // ---------------------------------------------------------------------------
 // One workgroup per tile.  The tile's segment is found by binary search over
 // the batch's tile prefix (kernel arguments, scalar loads); the tile's digest
-// share is reduced across the workgroup and added with one 64-bit atomic.
+// share is summed over the workgroup in LDS and added with one 64-bit atomic.
 // ---------------------------------------------------------------------------
 template <Mode M, typename A>
 __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t* lds) {
@@ -612,6 +620,13 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
     const uint64_t seg_first = bt.elem_begin[seg];
     const uint64_t seg_end = seg_first + bt.elem_count[seg];
     const uint64_t e0 = seg_first + (tile - bt.tile_begin[seg]) * (uint64_t)kTile;
+    // This wave's word of the workgroup sum starts at zero (LDS operations of
+    // one wave are carried out in the order it issues them, so the clearing
+    // comes before the wave's own additions below).
+    uint64_t* const wave_sum = lds + (threadIdx.x >> 6);
+    if ((threadIdx.x & 63) == 0) {
+        __hip_atomic_store(wave_sum, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
     uint64_t acc = 0;
     if (bt.vec_ok[seg] && e0 + kTile <= seg_end) {
         // The short index form for tiles that do not cross a multiple of
@@ -630,7 +645,19 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
             acc += do_scalar<M>(a, e, sc);
         }
     }
-    const uint64_t s = block_sum(acc, lds);
+    // Workgroup sum: every lane adds its share into its wave's LDS word with
+    // one 64-bit LDS atomic (no VALU work: a shuffle tree costs about fifty
+    // VALU instructions per lane, a few percent of a digesting kernel), then
+    // thread 0 adds the four words.
+    __hip_atomic_fetch_add(wave_sum, acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __syncthreads();
+    uint64_t s = 0;
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) {
+            s += lds[w];
+        }
+    }
     if (threadIdx.x == 0 && s != 0) {
         const uint64_t r = bt.per_segment ? bt.slot0 + seg : 0;
         uint64_t* dst = a.lanes ? a.lanes + (r * kLanes + (blockIdx.x & (kLanes - 1))) * kLaneStride : a.digest + r;
