@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 METRIC = "shard commit+digest elements/s and HBM GB/s (% of MI355X peak), 1 GPU"
 PEAK_HBM_GBPS = 8000.0
 PREWARM_S = 0.3  # seconds of read-only digest calls before the warm-up commits
+SETTLE_S = 0.2   # seconds each neighbouring kernel runs untimed before it is timed
 BYTES_PER_ELEM = 30  # read p, g, m, v (16) + write p', m', v' (12) + bf16 (2)
 KERNEL_SOURCES = ("paper_2609_18178_amd/csrc/kernels.hip", "paper_2609_18178_amd/csrc/launch.h")
 
@@ -493,7 +494,20 @@ def main():
     # guard (4 B/element) and the standalone state digest (12 B/element)
     extra = {}
     if not args.no_probe:
+        def settle(fn, seconds):
+            """Run fn back to back for `seconds` before it is timed: the shader
+            clock the power manager picks depends on what ran just before
+            (after the HBM-heavy commits it sits lower, and a VALU-bound kernel
+            timed right after them reads up to 10% slow), so each kernel is
+            timed at the clock its own steady run settles to."""
+            t_end = time.perf_counter() + seconds
+            while time.perf_counter() < t_end:
+                for _ in range(4):
+                    fn()
+                torch.cuda.synchronize()
+
         def time_call(fn, reps):
+            settle(fn, SETTLE_S)
             fn()
             torch.cuda.synchronize()
             s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -504,7 +518,8 @@ def main():
             torch.cuda.synchronize()
             return s_ev.elapsed_time(e_ev) / reps
 
-        def median_launch(fn, reps):
+        def median_launch(fn, reps, settle_s=0.0):
+            settle(fn, settle_s)
             fn()
             torch.cuda.synchronize()
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
@@ -584,8 +599,8 @@ def main():
                                          ("commit_bf16_state", (1 << 22, 1 << 24), 14, 8)):
             if name not in extra or n2 > n:
                 continue
-            t1 = median_launch(subshard_fn(name, n1), 40)
-            t2 = median_launch(subshard_fn(name, n2), 40)
+            t1 = median_launch(subshard_fn(name, n1), 40, settle_s=SETTLE_S / 2)
+            t2 = median_launch(subshard_fn(name, n2), 40, settle_s=SETTLE_S / 2)
             rate = (n2 - n1) / ((t2 - t1) / 1e3)
             full_ms = extra[name]["median_launch_ms"]
             ceil = {"elements_per_s": rate, "full_size_ms_at_ceiling": n / rate * 1e3,
