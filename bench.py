@@ -243,6 +243,10 @@ CLOCK_KERNELS = (("tile_kernel<(pact::Mode)0>", "commit", 30), ("probe_kernel(",
                  ("tile_kernel_bf16<(pact::Mode)5>", "commit_bf16_state", 14))
 XCDS = 8      # GRBM_GUI_ACTIVE comes back summed over the eight XCDs
 NUM_CUS = 256
+# Nominal VALU issue peak: 256 CUs x 4 SIMDs, each SIMD 16 lanes wide, so one
+# 64-lane wave-instruction per SIMD every 4 cycles, at 2.4 GHz.  gfx950
+# finishes some VALU instructions in fewer cycles, so a kernel can pass it.
+VALU_PEAK_WAVE_INSTR_PER_S = NUM_CUS * 4 * 16 / 64 * 2.4e9
 
 
 def record_clock(workload: str, clock_csv: str) -> dict:
@@ -667,6 +671,14 @@ def main():
 
     for name, entry in extra.items():
         entry["valu"] = valu_of(name)
+        if entry["valu"] is not None and "valu" in entry["bound"]:
+            wave_instr = entry["valu"]["instr_per_element"] * n / 64  # per launch
+            achieved_wi = wave_instr / (entry["median_launch_ms"] / 1e3)
+            entry["alu_roofline"] = {
+                "bound": "alu", "achieved": achieved_wi, "peak": VALU_PEAK_WAVE_INSTR_PER_S,
+                "unit": "VALU wave-instructions/s", "frac": achieved_wi / VALU_PEAK_WAVE_INSTR_PER_S,
+                "peak_derivation": "256 CUs x 4 SIMDs x 16 lanes per cycle / 64 lanes per wave-instruction x 2.4 GHz",
+                "instructions": "SQ_INSTS_VALU per element from the clock record x elements / 64, per launch"}
 
     parity = None
     all_steps = list(range(w.first_step, w.first_step + args.warmup + K))
