@@ -105,6 +105,39 @@ struct IndexAny {
     }
 };
 
+// The rest of the mix once the first round's product is known as
+// prod + (cross << 32) (prod the full 64-bit product of the low halves with
+// the first round's addend folded in, cross the low half of the cross
+// term): the high half takes cross with one VOP2 add, then the second
+// xor-shift and multiply and the final xor-shift.
+__device__ __forceinline__ uint64_t mix_after_first_round(uint64_t prod, uint32_t cross) {
+    uint32_t res_hi;
+    asm("v_add_u32_e32 %0, %1, %2" : "=v"(res_hi) : "v"((uint32_t)(prod >> 32)), "v"(cross));
+    uint64_t z = ((uint64_t)res_hi << 32) | (uint32_t)prod;
+    z = z ^ (z >> 27);
+    {
+        constexpr uint32_t c2lo = (uint32_t)kMul2, c2hi = (uint32_t)(kMul2 >> 32);
+        const uint32_t zl = (uint32_t)z, zh = (uint32_t)(z >> 32);
+        const uint32_t t = zl * c2hi;
+        uint64_t cr, pr, cy0, cy1;
+        asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cr), "=s"(cy0) : "v"(zh), "s"(c2lo), "v"(((uint64_t)zh << 32) | t));
+        asm("v_mad_u64_u32 %0, %1, %2, %3, 0" : "=v"(pr), "=s"(cy1) : "v"(zl), "s"(c2lo));
+        uint32_t rh;
+        asm("v_add_u32_e32 %0, %1, %2" : "=v"(rh) : "v"((uint32_t)(pr >> 32)), "v"((uint32_t)cr));
+        z = ((uint64_t)rh << 32) | (uint32_t)pr;
+    }
+    return z ^ (z >> 31);
+}
+
+// (h ^ (h >> 30)) * c mod 2^32 of wave-uniform h and c, on the scalar unit
+// (left to itself the compiler forms such per-tile constants with VALU
+// instructions, because their uses want VGPRs).
+__device__ __forceinline__ uint32_t scalar_xorshift30_mul(uint32_t h, uint32_t c) {
+    uint32_t r;
+    asm("s_lshr_b32 %0, %1, 30\n\ts_xor_b32 %0, %0, %1\n\ts_mul_i32 %0, %0, %2" : "=&s"(r) : "s"(h), "s"(c) : "scc");
+    return r;
+}
+
 // IndexHi32: for a tile whose indices all share their upper 32 bits `hi`
 // (every tile but one that crosses a multiple of 2^32).  With index = hi:lo
 // the word only meets the low half, so
@@ -140,14 +173,9 @@ struct IndexHi32 {
         for (uint32_t k = 0; k < 4; ++k) {
             const uint32_t h = (uint32_t)((high + kGamma + ((uint64_t)k << 56)) >> 32);
             const uint32_t h1 = h + 1u;
-            // Wave-uniform per tile: computed on the scalar unit (left to
-            // itself the compiler forms them with VALU instructions, because
-            // their uses below want VGPRs), then copied once into VGPRs.
-            uint32_t k0, k1;
-            asm("s_lshr_b32 %0, %1, 30\n\ts_xor_b32 %0, %0, %1\n\ts_mul_i32 %0, %0, %2"
-                : "=&s"(k0) : "s"(h), "s"(clo) : "scc");
-            asm("s_lshr_b32 %0, %1, 30\n\ts_xor_b32 %0, %0, %1\n\ts_mul_i32 %0, %0, %2"
-                : "=&s"(k1) : "s"(h1), "s"(clo) : "scc");
+            // wave-uniform per tile: scalar unit, then one copy into VGPRs
+            const uint32_t k0 = scalar_xorshift30_mul(h, clo);
+            const uint32_t k1 = scalar_xorshift30_mul(h1, clo);
             ghi[k] = h;
             kdiff[k] = k1 - k0;
             k0hi[k] = (uint64_t)k0 << 32;
@@ -176,22 +204,66 @@ struct IndexHi32 {
         asm("v_mad_u64_u32 %0, %1, %2, %3, %4"
             : "=v"(cross), "=s"(carry1)
             : "v"(lo1), "s"(chi), "v"(((uint64_t)zhi << 32) | ksel));
-        uint32_t res_hi;
-        asm("v_add_u32_e32 %0, %1, %2" : "=v"(res_hi) : "v"((uint32_t)(prod >> 32)), "v"((uint32_t)cross));
-        uint64_t z = ((uint64_t)res_hi << 32) | (uint32_t)prod;
-        z = z ^ (z >> 27);
-        {
-            constexpr uint32_t c2lo = (uint32_t)kMul2, c2hi = (uint32_t)(kMul2 >> 32);
-            const uint32_t zl = (uint32_t)z, zh = (uint32_t)(z >> 32);
-            const uint32_t t = zl * c2hi;
-            uint64_t cr, pr, cy0, cy1;
-            asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(cr), "=s"(cy0) : "v"(zh), "s"(c2lo), "v"(((uint64_t)zh << 32) | t));
-            asm("v_mad_u64_u32 %0, %1, %2, %3, 0" : "=v"(pr), "=s"(cy1) : "v"(zl), "s"(c2lo));
-            uint32_t rh;
-            asm("v_add_u32_e32 %0, %1, %2" : "=v"(rh) : "v"((uint32_t)(pr >> 32)), "v"((uint32_t)cr));
-            z = ((uint64_t)rh << 32) | (uint32_t)pr;
+        return mix_after_first_round(prod, (uint32_t)cross);
+    }
+};
+
+// IndexLo16: for a tile of 16-bit words (BF16 state, the bf16 working copy)
+// whose indices all share bits 16..63.  There x = word ^ lo = A + v with
+// A = lo & 0xFFFF0000 the same for the whole tile and v < 2^16, so with
+// B = A + G_lo = c0 * 2^32 + B_lo (wave-uniform):
+//   z_lo = x + G_lo = B_lo + v,   z_hi = G_hi + c0,
+// provided B_lo + v never carries out of 32 bits (B_lo <= 0xFFFF0000).  If
+// moreover no carry reaches bit 30 ((B_lo mod 2^30) <= 0x3FFF0000), the top
+// two bits of z_lo are those of B_lo, T = B_lo >> 30, so the first mixing
+// round is
+//   lo1 = z_lo ^ (T | z_hi << 2) = (x + G_lo) ^ U_k,   hi1 = H_k,
+//   z1  = lo1 * CLO + ((lo1 * CHI + H_k * CLO) << 32),
+// with U_k, H_k and K_k = H_k * CLO wave-uniform per tag: an add, an xor, a
+// multiply-add with the scalar addend K_k << 32, a multiply and an add, two
+// VOP3 instructions against three (and three fewer VALU instructions) in
+// IndexHi32, and no carry to pass.  The two checks fail only for A in
+// {0x00B50000, 0x40B50000, 0x80B50000, 0xC0B50000}; such a tile, and one that
+// crosses a multiple of 2^16, takes IndexHi32 or IndexAny.
+struct IndexLo16 {
+    static constexpr uint32_t kGammaLo = (uint32_t)kGamma;
+    uint32_t lo;       // low half of the lane's first index
+    uint32_t u[4];     // U_k per tag
+    uint64_t khi[4];   // K_k << 32 per tag
+    // Whether the tile of kTile indices from `first` on may take this form
+    // (wave-uniform).
+    static __device__ __forceinline__ bool applies(uint64_t first) {
+        if ((first >> 16) != ((first + kTile - 1) >> 16)) {
+            return false;
         }
-        return z ^ (z >> 31);
+        const uint32_t b_lo = ((uint32_t)first & 0xFFFF0000u) + kGammaLo;
+        return b_lo <= 0xFFFF0000u && (b_lo & 0x3FFFFFFFu) <= 0x3FFF0000u;
+    }
+    __device__ __forceinline__ IndexLo16(uint64_t tile_first, uint32_t lane_off)
+        : lo((uint32_t)tile_first + lane_off) {
+        constexpr uint32_t clo = (uint32_t)kMul1;
+        const uint64_t b = (uint64_t)((uint32_t)tile_first & 0xFFFF0000u) + kGammaLo;
+        const uint32_t c0 = (uint32_t)(b >> 32);
+        const uint32_t t = (uint32_t)b >> 30;
+        const uint32_t hi = (uint32_t)(tile_first >> 32);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k) {
+            const uint32_t zhi = hi + (uint32_t)(kGamma >> 32) + (k << 24) + c0;
+            u[k] = (zhi << 2) | t;
+            khi[k] = (uint64_t)scalar_xorshift30_mul(zhi, clo) << 32;
+        }
+    }
+    template <uint32_t Tag>
+    __device__ __forceinline__ uint64_t hash(uint32_t word, uint32_t off) const {
+        static_assert(Tag < 4, "array tags 0..3");
+        constexpr uint32_t clo = (uint32_t)kMul1, chi = (uint32_t)(kMul1 >> 32);
+        const uint32_t x = word ^ (lo + off);
+        uint32_t zlo;
+        asm("v_add_u32_e32 %0, %1, %2" : "=v"(zlo) : "s"(kGammaLo), "v"(x));
+        const uint32_t lo1 = zlo ^ u[Tag];
+        uint64_t prod, carry0;
+        asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(prod), "=s"(carry0) : "v"(lo1), "v"(clo), "s"(khi[Tag]));
+        return mix_after_first_round(prod, lo1 * chi);
     }
 };
 
@@ -371,6 +443,10 @@ __device__ __forceinline__ void store8(u32x2 x, __amdgpu_buffer_rsrc_t r, uint32
 // ---------------------------------------------------------------------------
 template <Mode M>
 constexpr bool kCommits = (M == Mode::Commit || M == Mode::CommitZeroGrad);
+
+// Modes whose digest words have 16 bits (the short IndexLo16 form applies).
+template <Mode M>
+constexpr bool kWords16 = (M == Mode::Bf16Digest || M == Mode::CommitBf16State || M == Mode::DigestBf16State);
 
 template <Mode M>
 __device__ __forceinline__ uint64_t do_scalar(const Arrays& a, uint64_t e, const StepScalars& sc) {
@@ -634,7 +710,9 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
         // the binary32 commits are bound by HBM, not by VALU issue, and keep
         // the plain form (the short one measured 0.3% slower there, with one
         // more wave per SIMD resident).
-        if (!kCommits<M> && same_high_half(a.goff + e0, kTile)) {
+        if (kWords16<M> && IndexLo16::applies(a.goff + e0)) {
+            acc = do_tile_vec<M, IndexLo16>(a, e0, sc);
+        } else if (!kCommits<M> && same_high_half(a.goff + e0, kTile)) {
             acc = do_tile_vec<M, IndexHi32>(a, e0, sc);
         } else {
             acc = do_tile_vec<M, IndexAny>(a, e0, sc);
@@ -669,9 +747,8 @@ __device__ __forceinline__ void tile_body(const A& a, const Batch& bt, uint64_t*
 // The two standalone digests are bound by VALU issue and keep the full
 // eight waves per SIMD (the short index form would otherwise take the state
 // digest to 66 VGPRs and seven waves).  The BF16-state commit, which holds
-// the moments of all its elements before the square roots, keeps five
-// (92 VGPRs; unbounded it takes 112 and four waves and measured 0.5% slower;
-// capped at six it spills).
+// the moments of all its elements before the square roots, needs at least
+// five; it takes 79 VGPRs, six waves (capped at seven it spills).
 template <Mode M>
 constexpr unsigned kMinWavesPerSimd = (M == Mode::StateDigest || M == Mode::DigestBf16State) ? 8u
                                       : (M == Mode::CommitBf16State)                         ? 5u

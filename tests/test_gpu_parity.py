@@ -228,6 +228,39 @@ def test_every_digest_across_index_halves(goff):
     assert pk.to_u64(pk.shard_digest_bf16(sh16))[0] == oracle.state_digest_bf16(pb, mb, vb, goff)
 
 
+@pytest.mark.parametrize("goff", [0x12340000 + 4096, 2 ** 16 - 1000, 0x80B50000 - 4096, (5 << 32) + 0x40B50000,
+                                  (7 << 32) + 0xC0B50000 - 2048, 0x00B50000, (3 << 40) + 0xFFFF0000 - 4096])
+def test_sixteen_bit_digests_at_every_index_form(goff):
+    """The digests of 16-bit words (BF16-state commit and digest, the bf16
+    copy's digest) take a short first mixing round on tiles whose indices
+    share bits 16..63, unless the low halves of those indices start at
+    0x00B50000, 0x40B50000, 0x80B50000 or 0xC0B50000 (where the short round's
+    carry assumptions fail).  Tiles of each kind -- short form, across a
+    multiple of 2^16, at each excluded start -- must give the oracle's
+    digests and state."""
+    import torch
+
+    pk = _pk()
+    w = wl.WORKLOADS["mistral7b_shard16"]
+    n = 3 * 4096 + 123
+    p, g, m, v = wl.arrays_host(w, 0, n)
+    sh = make_shard(p, g, m, v, goff)
+    b = np.zeros(n, np.uint16)
+    assert pk.to_u64(pk.adamw_commit(sh, 5, g_hyper(H)))[0] == oracle.commit_and_digest(
+        p, g, m, v, b, o_hyper(H), 5, goff)
+    assert_bitwise("bf16", host(sh.param_bf16).view(np.uint16), b)
+    assert pk.to_u64(pk.bf16_digest(sh))[0] == oracle.bf16_digest(b, goff)
+    pb, gb, mb, vb = _bf16_arrays(w, 0, n)
+    t = [torch.from_numpy(a.view(np.int16).copy()).cuda() for a in (pb, gb, mb, vb)]
+    sh16 = pk.ShardBf16(*t, global_offset=goff)
+    assert pk.to_u64(pk.shard_digest_bf16(sh16))[0] == oracle.state_digest_bf16(pb, mb, vb, goff)
+    got = pk.to_u64(pk.adamw_commit_bf16(sh16, 5, g_hyper(H)))[0]
+    assert got == oracle.commit_and_digest_bf16(pb, gb, mb, vb, o_hyper(H), 5, goff)
+    for name, tt, ref in (("param", sh16.param, pb), ("exp_avg", sh16.exp_avg, mb), ("exp_avg_sq", sh16.exp_avg_sq, vb)):
+        assert_bitwise(name, host(tt).view(np.uint16), ref)
+    assert pk.to_u64(pk.shard_digest_bf16(sh16))[0] == oracle.state_digest_bf16(pb, mb, vb, goff)
+
+
 def test_multi_segment_shrunken_mistral():
     """Real Mistral tensor roles at a small size with padding, four hyper
     sets (norms without decay, lm_head with its own beta2): per-segment
