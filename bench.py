@@ -599,22 +599,27 @@ def main():
                 st[0] += 1
             return f
 
-        for name, (n1, n2), bpe, ws in (("shard_digest", (1 << 22, 1 << 24), 12, 12),
-                                         ("commit_bf16_state", (1 << 22, 1 << 24), 14, 8)):
-            if name not in extra or n2 > n:
+        sub_sizes = (1 << 22, 2 << 22, 3 << 22, 4 << 22)
+        for name, bpe, ws in (("shard_digest", 12, 12), ("commit_bf16_state", 14, 8)):
+            if name not in extra or sub_sizes[-1] > n:
                 continue
-            t1 = median_launch(subshard_fn(name, n1), 40, settle_s=SETTLE_S / 2)
-            t2 = median_launch(subshard_fn(name, n2), 40, settle_s=SETTLE_S / 2)
-            rate = (n2 - n1) / ((t2 - t1) / 1e3)
+            ts = [median_launch(subshard_fn(name, m), 40, settle_s=SETTLE_S / 2) for m in sub_sizes]
+            # least-squares slope of launch time over elements: the fixed
+            # launch and tail costs drop out, and four sizes average the noise
+            # of any one median
+            mx, my = sum(sub_sizes) / len(ts), sum(ts) / len(ts)
+            slope = (sum((x - mx) * (y - my) for x, y in zip(sub_sizes, ts))
+                     / sum((x - mx) ** 2 for x in sub_sizes))  # ms per element
+            rate = 1e3 / slope
             full_ms = extra[name]["median_launch_ms"]
             ceil = {"elements_per_s": rate, "full_size_ms_at_ceiling": n / rate * 1e3,
                     "frac": (n / rate * 1e3) / full_ms,
                     "bytes_per_s_at_ceiling": rate * bpe,
-                    "sizes": [n1, n2], "median_launch_ms": [t1, t2],
-                    "working_set_bytes": n2 * ws,
-                    "method": "slope of the median launch time between two cache-resident sub-shards "
-                              "(same kernel, same instruction mix); frac = full-size time at that rate / "
-                              "measured full-size median launch time"}
+                    "sizes": list(sub_sizes), "median_launch_ms": ts,
+                    "working_set_bytes": sub_sizes[-1] * ws,
+                    "method": "least-squares slope of the median launch time over four cache-resident "
+                              "sub-shards (same kernel, same instruction mix); frac = full-size time at that "
+                              "rate / measured full-size median launch time"}
             extra[name]["valu_ceiling"] = ceil
             print(f"[bench] {name}: cache-resident rate {rate:.3e} elem/s -> {n / rate * 1e3:.4f} ms at full size, "
                   f"frac {ceil['frac']:.3f} of that ceiling", file=sys.stderr, flush=True)
